@@ -1,0 +1,144 @@
+// C ABI of libtacg: host-side argument validation, then enqueue on the caller's stream.
+// Argument errors return before any HIP call, so they can be exercised on a machine without a GPU.
+#include <cstdint>
+
+#include "tacg_internal.h"
+
+namespace {
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Common trace checks: shapes, limits and the family offsets.
+int check_trace(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+                const int64_t* fam_off_host, int32_t n_fam) {
+  if (n_tokens < 0 || n_layers < 1 || n_fam < 1 || n_experts < 1 || top_k < 1) return TACG_E_INVAL;
+  if (top_k > n_experts) return TACG_E_INVAL;
+  if (n_experts > TACG_MAX_EXPERTS || top_k > TACG_MAX_TOPK || n_fam > TACG_MAX_FAMILIES) return TACG_E_UNSUPPORTED;
+  if (n_tokens * static_cast<int64_t>(top_k) >= (int64_t(1) << 32)) return TACG_E_UNSUPPORTED;
+  if (n_tokens > 0 && (trace == nullptr || !aligned(trace, 16))) return TACG_E_INVAL;
+  if (fam_off_host == nullptr) return TACG_E_INVAL;
+  if (fam_off_host[0] != 0 || fam_off_host[n_fam] != n_tokens) return TACG_E_INVAL;
+  for (int f = 0; f < n_fam; ++f)
+    if (fam_off_host[f + 1] < fam_off_host[f]) return TACG_E_INVAL;
+  return TACG_OK;
+}
+
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+size_t tacg_coact_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+                                  int32_t n_fam) {
+  if (n_tokens < 0 || n_layers < 1 || top_k < 1 || n_experts < 1 || n_fam < 1) return 0;
+  const int64_t total = n_tokens * n_layers;
+  const int64_t W = tacg::coact_num_workgroups(total, n_experts);
+  const size_t slots = static_cast<size_t>(W) + static_cast<size_t>(n_layers) * n_fam;
+  return tacg::align256(slots * tacg::coact_bins(n_experts, top_k) * sizeof(uint32_t));
+}
+
+int tacg_coact_build(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+                     const int64_t* fam_off_host, int32_t n_fam, uint32_t* D, uint32_t* C, uint32_t flags,
+                     uint32_t* d_err, void* workspace, size_t workspace_bytes, void* hip_stream) {
+  int rc = check_trace(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam);
+  if (rc != TACG_OK) return rc;
+  if (D == nullptr || C == nullptr || d_err == nullptr) return TACG_E_INVAL;
+  if ((flags & ~TACG_ACCUMULATE) != 0) return TACG_E_INVAL;
+  const size_t need = tacg_coact_workspace_bytes(n_tokens, n_layers, top_k, n_experts, n_fam);
+  if (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 256)) return TACG_E_INVAL;
+  return tacg::launch_coact(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, D, C, flags, d_err,
+                            workspace, as_stream(hip_stream));
+}
+
+size_t tacg_reweight_workspace_bytes(int32_t n_fam, int32_t n_layers, int32_t n_experts) {
+  if (n_fam < 1 || n_layers < 1 || n_experts < 1) return 0;
+  return tacg::reweight_workspace(n_fam, n_layers, n_experts);
+}
+
+int tacg_reweight(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t n_layers, int32_t n_experts,
+                  int32_t top_k, double alpha, double tau, double eps, float* pref, float* a_tilde,
+                  float* a_hat_or_null, void* workspace, size_t workspace_bytes, void* hip_stream) {
+  if (D == nullptr || C == nullptr || pref == nullptr || a_tilde == nullptr) return TACG_E_INVAL;
+  if (n_fam < 2 || n_layers < 1 || n_experts < 1 || top_k < 1 || top_k > n_experts) return TACG_E_INVAL;
+  if (n_experts > TACG_MAX_EXPERTS || n_fam > TACG_MAX_FAMILIES || top_k > TACG_MAX_TOPK) return TACG_E_UNSUPPORTED;
+  if (!(alpha >= 0.0 && alpha <= 1.0) || !(tau > 0.0) || !(eps >= 0.0)) return TACG_E_INVAL;
+  const size_t need = tacg_reweight_workspace_bytes(n_fam, n_layers, n_experts);
+  if (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 256)) return TACG_E_INVAL;
+  return tacg::launch_reweight(D, C, n_fam, n_layers, n_experts, top_k, alpha, tau, eps, pref, a_tilde,
+                               a_hat_or_null, workspace, as_stream(hip_stream));
+}
+
+int tacg_placement_load(const uint32_t* D, int32_t n_fam, int32_t n_layers, int32_t n_experts,
+                        const uint8_t* primary, int32_t n_place, int32_t n_gpus, int64_t* load_ref, uint32_t* d_err,
+                        void* hip_stream) {
+  if (D == nullptr || primary == nullptr || load_ref == nullptr || d_err == nullptr) return TACG_E_INVAL;
+  if (n_fam < 1 || n_layers < 1 || n_experts < 1 || n_place < 0 || n_gpus < 1) return TACG_E_INVAL;
+  if (n_experts > TACG_MAX_EXPERTS || n_fam > TACG_MAX_FAMILIES || n_gpus > TACG_MAX_GPUS) return TACG_E_UNSUPPORTED;
+  if (n_place == 0) return TACG_OK;
+  return tacg::launch_placement_load(D, n_fam, n_layers, n_experts, primary, n_place, n_gpus, load_ref, d_err,
+                                     as_stream(hip_stream));
+}
+
+size_t tacg_eval_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t n_experts, int32_t n_gpus,
+                                 int32_t n_place, int32_t n_fam) {
+  if (n_tokens < 0 || n_layers < 1 || n_experts < 1 || n_gpus < 1 || n_place < 1 || n_fam < 1) return 0;
+  return tacg::eval_workspace(n_tokens, n_layers, n_experts, n_gpus, n_place, n_fam);
+}
+
+int tacg_eval_placements(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
+                         int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam,
+                         const int32_t* home_start_host, const int32_t* home_size_host, int32_t n_gpus,
+                         int32_t n_place, const uint8_t* primary, const uint8_t* secondary_or_null, int32_t n_sec,
+                         const int64_t* load_ref_or_null, int32_t theta_num, int32_t theta_den,
+                         uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
+                         uint64_t* cost_home_fam_or_null, uint32_t flags, uint32_t* d_err, void* workspace,
+                         size_t workspace_bytes, void* hip_stream) {
+  int rc = check_trace(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam);
+  if (rc != TACG_OK) return rc;
+  if (flags != 0) return TACG_E_INVAL;
+  if (n_gpus < 1 || n_place < 1 || n_sec < 0) return TACG_E_INVAL;
+  if (n_gpus > TACG_MAX_GPUS || n_sec > TACG_MAX_SECONDARY) return TACG_E_UNSUPPORTED;
+  if (primary == nullptr || cost_home == nullptr || cost_span == nullptr || load == nullptr || d_err == nullptr)
+    return TACG_E_INVAL;
+  if (n_sec > 0 && (secondary_or_null == nullptr || load_ref_or_null == nullptr)) return TACG_E_INVAL;
+  if (theta_num < 0 || theta_den < 0 || (theta_den > 0 && theta_num > (1 << 20)) || theta_den > (1 << 20))
+    return TACG_E_INVAL;
+  if (home_start_host == nullptr || home_size_host == nullptr) return TACG_E_INVAL;
+  for (int f = 0; f < n_fam; ++f) {
+    if (home_size_host[f] < 1 || home_start_host[f] < 0 || home_start_host[f] + home_size_host[f] > n_gpus)
+      return TACG_E_INVAL;
+  }
+  const size_t need = tacg_eval_workspace_bytes(n_tokens, n_layers, n_experts, n_gpus, n_place, n_fam);
+  if (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 256)) return TACG_E_INVAL;
+  return tacg::launch_eval(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, home_start_host,
+                           home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec, load_ref_or_null,
+                           theta_num, theta_den, cost_home, cost_span, load, cost_home_fam_or_null, d_err, workspace,
+                           as_stream(hip_stream));
+}
+
+int tacg_jain(const uint32_t* load, int32_t n_place, int32_t n_layers, int32_t n_gpus, int32_t per_layer,
+              float* jain, float* maxvio, void* hip_stream) {
+  if (load == nullptr || jain == nullptr || maxvio == nullptr) return TACG_E_INVAL;
+  if (n_place < 0 || n_layers < 1 || n_gpus < 1 || (per_layer != 0 && per_layer != 1)) return TACG_E_INVAL;
+  if (n_gpus > TACG_MAX_GPUS) return TACG_E_UNSUPPORTED;
+  if (n_place == 0) return TACG_OK;
+  return tacg::launch_jain(load, n_place, n_layers, n_gpus, per_layer, jain, maxvio, as_stream(hip_stream));
+}
+
+const char* tacg_strerror(int status) {
+  switch (status) {
+    case TACG_OK:
+      return "ok";
+    case TACG_E_INVAL:
+      return "invalid argument";
+    case TACG_E_UNSUPPORTED:
+      return "argument beyond a supported limit";
+    case TACG_E_DEVICE:
+      return "HIP launch failed";
+    default:
+      return "unknown status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,216 @@
+// Family preferences and the task-modulated co-activation graph (Sec. 3.3, eqs.
+// usage-coact-advantage, coact-advantage, zscore, soft-score, family-pref, same-family-kernel,
+// task-modulated-graph).  Internal arithmetic is float64; outputs are float32.
+//
+// Three passes per call (all tiny next to the trace passes; C is read once):
+//   rw_rows   grid (L, row blocks): per row i and family f the co-activation strength
+//             c_f(i) = sum_{j != i} C_f[i][j] / N_f, the pooled A-bar[i][j] = mean_f C_f[i][j] / N_f
+//             (zero diagonal) and the layer maximum of A-bar (atomic max on the float64 bit pattern,
+//             valid because every value is >= 0).
+//   rw_pref   grid (L): usage u_f = D_f / (N_f k), advantages against the mean of the other
+//             families, z-scores over experts (population std), s = z(du) + z(dc), softmax over f.
+//   rw_graph  grid (L, row blocks): A-hat = A-bar / max, A_task = P P^T, A-tilde.
+#include "tacg_internal.h"
+
+namespace tacg {
+namespace {
+
+constexpr int kRows = 16;  // rows of a layer per workgroup in rw_rows / rw_graph
+
+struct RwWs {
+  double* c;          // [L][F][E]
+  double* abar;       // [L][E][E]
+  uint64_t* maxbits;  // [L]
+  double* s;          // [L][F][E]  soft scores
+  double* p;          // [L][F][E]  preferences
+};
+
+RwWs carve_rw(void* ws, int32_t F, int32_t L, int32_t E, size_t* used = nullptr) {
+  Carver c{static_cast<char*>(ws), 0};
+  RwWs r;
+  r.c = c.take<double>(static_cast<size_t>(L) * F * E);
+  r.abar = c.take<double>(static_cast<size_t>(L) * E * E);
+  r.maxbits = c.take<uint64_t>(static_cast<size_t>(L));
+  r.s = c.take<double>(static_cast<size_t>(L) * F * E);
+  r.p = c.take<double>(static_cast<size_t>(L) * F * E);
+  if (used) *used = c.used;
+  return r;
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ double wave_max(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Sum over the workgroup (blockDim.x a multiple of 64, <= 1024); every thread gets the result.
+__device__ double block_sum(double v, double* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  double t = 0.0;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  return t;
+}
+
+// tokens of family f at layer l: sum_i D[f][l][i] / k
+__device__ double family_tokens(const uint32_t* D, int f, int l, int L, int E, int k) {
+  const uint32_t* d = D + (static_cast<int64_t>(f) * L + l) * E;
+  uint64_t s = 0;
+  for (int i = 0; i < E; ++i) s += d[i];
+  return static_cast<double>(s) / k;
+}
+
+__global__ __launch_bounds__(256) void rw_init(uint64_t* maxbits, int L) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < L) maxbits[i] = 0;
+}
+
+__global__ __launch_bounds__(256) void rw_rows(const uint32_t* __restrict__ D, const uint32_t* __restrict__ C,
+                                                int F, int L, int E, int k, RwWs ws) {
+  __shared__ double inv_n[TACG_MAX_FAMILIES];
+  const int l = blockIdx.x;
+  if (threadIdx.x < F) {
+    const double n = family_tokens(D, threadIdx.x, l, L, E, k);
+    inv_n[threadIdx.x] = n > 0 ? 1.0 / n : 0.0;
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int r0 = blockIdx.y * kRows, r1 = min(E, r0 + kRows);
+  double mx = 0.0;
+  for (int i = r0 + wave; i < r1; i += nw) {
+    double ab[4] = {0, 0, 0, 0};
+    for (int f = 0; f < F; ++f) {
+      const uint32_t* row = C + ((static_cast<int64_t>(f) * L + l) * E + i) * E;
+      double rs = 0.0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = lane + 64 * q;
+        if (j < E && j != i) {
+          const double a = row[j] * inv_n[f];
+          rs += a;
+          ab[q] += a;
+        }
+      }
+      rs = wave_sum(rs);
+      if (lane == 0) ws.c[(static_cast<int64_t>(l) * F + f) * E + i] = rs;
+    }
+    double* arow = ws.abar + (static_cast<int64_t>(l) * E + i) * E;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = lane + 64 * q;
+      if (j < E) {
+        const double v = ab[q] / F;
+        arow[j] = v;
+        mx = fmax(mx, v);
+      }
+    }
+  }
+  mx = wave_max(mx);
+  if (lane == 0 && mx > 0.0) atomicMax(reinterpret_cast<unsigned long long*>(ws.maxbits + l),
+                                       static_cast<unsigned long long>(__double_as_longlong(mx)));
+}
+
+// One workgroup per layer, one thread per expert (E <= 256 = blockDim).
+__global__ __launch_bounds__(256) void rw_pref(const uint32_t* __restrict__ D, int F, int L, int E, int k,
+                                               double tau, double eps, float* __restrict__ pref, RwWs ws) {
+  __shared__ double red[16];
+  __shared__ double nf[TACG_MAX_FAMILIES];
+  const int l = blockIdx.x;
+  const int e = threadIdx.x;
+  const bool on = e < E;
+  if (threadIdx.x < F) nf[threadIdx.x] = family_tokens(D, threadIdx.x, l, L, E, k);
+  __syncthreads();
+  // sums over families of u and c for this expert
+  double su = 0.0, sc = 0.0;
+  if (on) {
+    for (int f = 0; f < F; ++f) {
+      const double n = nf[f];
+      su += n > 0 ? D[(static_cast<int64_t>(f) * L + l) * E + e] / (n * k) : 0.0;
+      sc += ws.c[(static_cast<int64_t>(l) * F + f) * E + e];
+    }
+  }
+  for (int f = 0; f < F; ++f) {
+    const double n = nf[f];
+    double du = 0.0, dc = 0.0;
+    if (on) {
+      const double u = n > 0 ? D[(static_cast<int64_t>(f) * L + l) * E + e] / (n * k) : 0.0;
+      const double c = ws.c[(static_cast<int64_t>(l) * F + f) * E + e];
+      du = u - (su - u) / (F - 1);
+      dc = c - (sc - c) / (F - 1);
+    }
+    const double mu_u = block_sum(on ? du : 0.0, red) / E;
+    const double mu_c = block_sum(on ? dc : 0.0, red) / E;
+    const double vu = block_sum(on ? (du - mu_u) * (du - mu_u) : 0.0, red) / E;
+    const double vc = block_sum(on ? (dc - mu_c) * (dc - mu_c) : 0.0, red) / E;
+    if (on) {
+      const double s = (du - mu_u) / (sqrt(vu) + eps) + (dc - mu_c) / (sqrt(vc) + eps);
+      ws.s[(static_cast<int64_t>(l) * F + f) * E + e] = s / tau;
+    }
+  }
+  if (!on) return;
+  double zmax = -INFINITY;
+  for (int f = 0; f < F; ++f) zmax = fmax(zmax, ws.s[(static_cast<int64_t>(l) * F + f) * E + e]);
+  double den = 0.0;
+  for (int f = 0; f < F; ++f) den += exp(ws.s[(static_cast<int64_t>(l) * F + f) * E + e] - zmax);
+  for (int f = 0; f < F; ++f) {
+    const double p = exp(ws.s[(static_cast<int64_t>(l) * F + f) * E + e] - zmax) / den;
+    ws.p[(static_cast<int64_t>(l) * F + f) * E + e] = p;
+    pref[(static_cast<int64_t>(l) * E + e) * F + f] = static_cast<float>(p);
+  }
+}
+
+__global__ __launch_bounds__(256) void rw_graph(int F, int L, int E, double alpha, float* __restrict__ a_tilde,
+                                                float* __restrict__ a_hat, RwWs ws) {
+  const int l = blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const double mx = __longlong_as_double(static_cast<long long>(ws.maxbits[l]));
+  const double inv = mx > 0.0 ? 1.0 / mx : 0.0;
+  const int r0 = blockIdx.y * kRows, r1 = min(E, r0 + kRows);
+  const double* P = ws.p + static_cast<int64_t>(l) * F * E;  // [F][E]
+  for (int i = r0 + wave; i < r1; i += nw) {
+    const double* arow = ws.abar + (static_cast<int64_t>(l) * E + i) * E;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = lane + 64 * q;
+      if (j >= E) continue;
+      const double ah = mx > 0.0 ? arow[j] * inv : 0.0;
+      double task = 0.0;
+      for (int f = 0; f < F; ++f) task += P[f * E + i] * P[f * E + j];
+      const double at = (1.0 - alpha) * ah + alpha * (task * ah);
+      const int64_t o = (static_cast<int64_t>(l) * E + i) * E + j;
+      a_tilde[o] = static_cast<float>(at);
+      if (a_hat) a_hat[o] = static_cast<float>(ah);
+    }
+  }
+}
+
+}  // namespace
+
+size_t reweight_workspace(int32_t F, int32_t L, int32_t E) {
+  size_t used = 0;
+  carve_rw(nullptr, F, L, E, &used);
+  return used;
+}
+
+int launch_reweight(const uint32_t* D, const uint32_t* C, int32_t F, int32_t L, int32_t E, int32_t k,
+                    double alpha, double tau, double eps, float* pref, float* a_tilde, float* a_hat,
+                    void* workspace, hipStream_t stream) {
+  RwWs ws = carve_rw(workspace, F, L, E);
+  const int rb = (E + kRows - 1) / kRows;
+  hipLaunchKernelGGL(rw_init, dim3((L + 255) / 256), dim3(256), 0, stream, ws.maxbits, L);
+  hipLaunchKernelGGL(rw_rows, dim3(L, rb), dim3(256), 0, stream, D, C, F, L, E, k, ws);
+  hipLaunchKernelGGL(rw_pref, dim3(L), dim3(256), 0, stream, D, F, L, E, k, tau, eps, pref, ws);
+  hipLaunchKernelGGL(rw_graph, dim3(L, rb), dim3(256), 0, stream, F, L, E, alpha, a_tilde, a_hat, ws);
+  return hipGetLastError() == hipSuccess ? TACG_OK : TACG_E_DEVICE;
+}
+
+}  // namespace tacg

@@ -1,0 +1,57 @@
+// Internal declarations shared by the HIP translation units of libtacg (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "tacg.h"
+
+namespace tacg {
+
+// Round a byte count up to the 256-byte alignment used for every workspace sub-buffer.
+inline size_t align256(size_t x) { return (x + 255u) & ~size_t(255); }
+
+// Bump allocator over a caller-provided workspace (device memory).  Only carves offsets.
+struct Carver {
+  char* base;
+  size_t used;
+  template <class T>
+  T* take(size_t count) {
+    T* p = reinterpret_cast<T*>(base ? base + used : nullptr);
+    used += align256(count * sizeof(T));
+    return p;
+  }
+};
+
+// ---- co-activation build -------------------------------------------------------------------
+constexpr int kCoactThreads = 1024;
+int coact_num_workgroups(int64_t total_token_layers, int32_t n_experts);
+size_t coact_bins(int32_t n_experts, int32_t top_k);
+
+int launch_coact(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+                 const int64_t* fam_off_host, int32_t n_fam, uint32_t* D, uint32_t* C, uint32_t flags,
+                 uint32_t* d_err, void* workspace, hipStream_t stream);
+
+// ---- reweighting ---------------------------------------------------------------------------
+size_t reweight_workspace(int32_t n_fam, int32_t n_layers, int32_t n_experts);
+int launch_reweight(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t n_layers, int32_t n_experts,
+                    int32_t top_k, double alpha, double tau, double eps, float* pref, float* a_tilde,
+                    float* a_hat, void* workspace, hipStream_t stream);
+
+// ---- placement scoring ---------------------------------------------------------------------
+size_t eval_workspace(int64_t n_tokens, int32_t n_layers, int32_t n_experts, int32_t n_gpus, int32_t n_place,
+                      int32_t n_fam);
+int launch_eval(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+                const int64_t* fam_off_host, int32_t n_fam, const int32_t* home_start_host,
+                const int32_t* home_size_host, int32_t n_gpus, int32_t n_place, const uint8_t* primary,
+                const uint8_t* secondary, int32_t n_sec, const int64_t* load_ref, int32_t theta_num,
+                int32_t theta_den, uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
+                uint64_t* cost_home_fam, uint32_t* d_err, void* workspace, hipStream_t stream);
+int launch_placement_load(const uint32_t* D, int32_t n_fam, int32_t n_layers, int32_t n_experts,
+                          const uint8_t* primary, int32_t n_place, int32_t n_gpus, int64_t* load_ref,
+                          uint32_t* d_err, hipStream_t stream);
+int launch_jain(const uint32_t* load, int32_t n_place, int32_t n_layers, int32_t n_gpus, int32_t per_layer,
+                float* jain, float* maxvio, hipStream_t stream);
+
+}  // namespace tacg

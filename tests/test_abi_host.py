@@ -1,0 +1,147 @@
+"""Host-side checks of the C ABI (CPU only): the library loads, exports every function that
+include/tacg.h declares, sizes its workspaces, and rejects bad arguments before touching a device."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2606_01007_amd as tacg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tacg.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tacg_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(tacg.LIB_PATH):
+        pytest.skip("libtacg.so not built")
+    return tacg.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = _declared()
+    assert {"tacg_coact_build", "tacg_reweight", "tacg_eval_placements", "tacg_jain"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_strerror(L):
+    for code in (0, -1, -2, -3, 7):
+        assert isinstance(L.tacg_strerror(code), bytes)
+
+
+def test_workspace_sizes(L):
+    # coact: (W + L*F) slots of the triangle; at E = 256 one workgroup per CU (256)
+    tri = 256 * 255 // 2
+    n = L.tacg_coact_workspace_bytes(1 << 23, 58, 8, 256, 16)
+    assert n >= (256 + 58 * 16) * tri * 4 and n % 256 == 0
+    assert L.tacg_coact_workspace_bytes(6144, 2, 2, 8, 3) >= 3 * 2 * 28 * 4
+    assert L.tacg_coact_workspace_bytes(-1, 2, 2, 8, 3) == 0
+    assert L.tacg_reweight_workspace_bytes(16, 58, 256) >= 58 * 256 * 256 * 8
+    assert L.tacg_eval_workspace_bytes(1 << 23, 58, 256, 32, 1024, 16) > 0
+    assert L.tacg_eval_workspace_bytes(10, 0, 8, 4, 1, 1) == 0
+
+
+FAKE = ctypes.c_void_p(1 << 20)   # never dereferenced: every call below fails validation first
+
+
+def _coact(L, **kw):
+    a = dict(trace=FAKE, N=100, Ly=2, k=2, E=8, off=np.array([0, 50, 100], dtype=np.int64), F=2, D=FAKE, C=FAKE,
+             flags=0, err=FAKE, ws=FAKE, wsb=1 << 30)
+    a.update(kw)
+    return L.tacg_coact_build(a["trace"], a["N"], a["Ly"], a["k"], a["E"],
+                              a["off"].ctypes.data_as(ctypes.c_void_p) if a["off"] is not None else None,
+                              a["F"], a["D"], a["C"], a["flags"], a["err"], a["ws"], a["wsb"], None)
+
+
+def test_coact_argument_errors(L):
+    assert _coact(L, Ly=0) == tacg.E_INVAL
+    assert _coact(L, k=9) == tacg.E_INVAL                       # k > E
+    assert _coact(L, E=300, k=2) == tacg.E_UNSUPPORTED
+    assert _coact(L, k=17, E=32) == tacg.E_UNSUPPORTED
+    assert _coact(L, off=np.array([0, 60, 50], dtype=np.int64)) == tacg.E_INVAL   # not monotone / end != N
+    assert _coact(L, off=np.array([0, 60, 99], dtype=np.int64)) == tacg.E_INVAL
+    assert _coact(L, off=np.array([1, 60, 100], dtype=np.int64)) == tacg.E_INVAL
+    assert _coact(L, off=None) == tacg.E_INVAL
+    assert _coact(L, trace=None) == tacg.E_INVAL
+    assert _coact(L, trace=ctypes.c_void_p((1 << 20) + 2)) == tacg.E_INVAL   # misaligned trace
+    assert _coact(L, D=None) == tacg.E_INVAL
+    assert _coact(L, err=None) == tacg.E_INVAL
+    assert _coact(L, flags=4) == tacg.E_INVAL
+    assert _coact(L, wsb=16) == tacg.E_INVAL
+    assert _coact(L, ws=ctypes.c_void_p((1 << 20) + 64)) == tacg.E_INVAL   # workspace not 256-aligned
+    assert _coact(L, N=1 << 31, k=2, off=np.array([0, 1 << 30, 1 << 31], dtype=np.int64)) == tacg.E_UNSUPPORTED
+    assert _coact(L, F=65, off=np.zeros(66, dtype=np.int64)) in (tacg.E_UNSUPPORTED, tacg.E_INVAL)
+
+
+def test_reweight_argument_errors(L):
+    f = L.tacg_reweight
+    ok = dict(D=FAKE, C=FAKE, F=3, Ly=2, E=8, k=2, alpha=0.25, tau=1.0, eps=1e-8, pref=FAKE, at=FAKE, ah=None,
+              ws=FAKE, wsb=1 << 30)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return f(a["D"], a["C"], a["F"], a["Ly"], a["E"], a["k"], a["alpha"], a["tau"], a["eps"], a["pref"],
+                 a["at"], a["ah"], a["ws"], a["wsb"], None)
+
+    assert call(F=1) == tacg.E_INVAL
+    assert call(alpha=1.5) == tacg.E_INVAL
+    assert call(tau=0.0) == tacg.E_INVAL
+    assert call(eps=-1.0) == tacg.E_INVAL
+    assert call(D=None) == tacg.E_INVAL
+    assert call(wsb=8) == tacg.E_INVAL
+    assert call(E=512) == tacg.E_UNSUPPORTED
+
+
+def test_eval_argument_errors(L):
+    off = np.array([0, 60, 100], dtype=np.int64)
+    hs = np.array([0, 2], dtype=np.int32)
+    hz = np.array([2, 2], dtype=np.int32)
+
+    def call(G=4, P=3, R=0, sec=None, ref=None, hs_=hs, hz_=hz, flags=0, tn=3, td=20, wsb=1 << 30, off_=off):
+        return L.tacg_eval_placements(FAKE, 100, 2, 2, 8, off_.ctypes.data_as(ctypes.c_void_p), 2,
+                                      hs_.ctypes.data_as(ctypes.c_void_p), hz_.ctypes.data_as(ctypes.c_void_p),
+                                      G, P, FAKE, sec, R, ref, tn, td, FAKE, FAKE, FAKE, None, flags, FAKE, FAKE,
+                                      wsb, None)
+
+    assert call(G=33) == tacg.E_UNSUPPORTED
+    assert call(G=0) == tacg.E_INVAL
+    assert call(P=0) == tacg.E_INVAL
+    assert call(R=5, sec=FAKE, ref=FAKE) == tacg.E_UNSUPPORTED
+    assert call(R=2, sec=None, ref=FAKE) == tacg.E_INVAL
+    assert call(R=2, sec=FAKE, ref=None) == tacg.E_INVAL
+    assert call(hz_=np.array([2, 0], dtype=np.int32)) == tacg.E_INVAL
+    assert call(hs_=np.array([0, 3], dtype=np.int32)) == tacg.E_INVAL     # band past G
+    assert call(flags=1) == tacg.E_INVAL
+    assert call(tn=-1) == tacg.E_INVAL
+    assert call(wsb=1) == tacg.E_INVAL
+    assert call(off_=np.array([0, 60, 90], dtype=np.int64)) == tacg.E_INVAL
+
+
+def test_jain_and_load_argument_errors(L):
+    assert L.tacg_jain(FAKE, 2, 1, 33, 0, FAKE, FAKE, None) == tacg.E_UNSUPPORTED
+    assert L.tacg_jain(FAKE, 2, 1, 4, 2, FAKE, FAKE, None) == tacg.E_INVAL
+    assert L.tacg_jain(None, 2, 1, 4, 0, FAKE, FAKE, None) == tacg.E_INVAL
+    assert L.tacg_jain(FAKE, 0, 1, 4, 0, FAKE, FAKE, None) == tacg.OK        # nothing to do
+    assert L.tacg_placement_load(FAKE, 2, 2, 8, FAKE, 3, 40, FAKE, FAKE, None) == tacg.E_UNSUPPORTED
+    assert L.tacg_placement_load(None, 2, 2, 8, FAKE, 3, 4, FAKE, FAKE, None) == tacg.E_INVAL
+
+
+def test_binding_refuses_host_tensors():
+    import torch
+    if not os.path.exists(tacg.LIB_PATH):
+        pytest.skip("libtacg.so not built")
+    tr = torch.zeros((1, 4, 2), dtype=torch.int16)
+    with pytest.raises(ValueError):
+        tacg.coact_build(tr, [0, 4], 8, D=torch.zeros((1, 1, 8), dtype=torch.int32),
+                         C=torch.zeros((1, 1, 8, 8), dtype=torch.int32), ws=torch.zeros(1 << 12, dtype=torch.uint8),
+                         err=torch.zeros(1, dtype=torch.int32))

@@ -1,0 +1,287 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle on the same seeded inputs.
+
+Integer outputs (counts, costs, loads) must match bit for bit; preferences, reweighted edges and
+Jain / MaxVio (float32 from float64 device arithmetic) within 1e-5 relative of the float64 oracle.
+The oracle always computes from the trace itself (its inputs never come from the HIP path).
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_01007_amd as tacg
+from paper_2606_01007_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+RTOL = 1e-5
+ATOL = 1e-30
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    if not os.path.exists(tacg.LIB_PATH):
+        pytest.fail("libtacg.so is not built")
+    oracle.build()
+
+
+def _u32(t):
+    return tacg.as_u32(t).cpu().numpy()
+
+
+def _err(e):
+    torch.cuda.synchronize()
+    return int(e.item()) & 0xFFFFFFFF
+
+
+def _rand_trace(L, N, k, E, seed, device="cuda"):
+    g = torch.Generator(device="cpu").manual_seed(seed)
+    x = torch.rand((L, N, E), generator=g)
+    return torch.topk(x, k, dim=2).indices.to(torch.int16).to(device)
+
+
+# ------------------------------------------------------------------------------------------------
+# co-activation counts
+# ------------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("E,k,L,counts,seed", [
+    (8, 2, 2, [2048, 2048, 2048], 1),
+    (60, 4, 3, [5000, 0, 3001, 777], 2),
+    (64, 6, 2, [4096, 9000], 3),
+    (13, 1, 2, [300, 200], 4),
+    (37, 5, 2, [1000, 1], 5),
+    (128, 8, 2, [3333, 4444], 6),
+    (256, 8, 2, [5000, 7000, 11], 7),
+    (256, 16, 1, [2000], 8),
+    (200, 3, 3, [4000, 4000], 9),
+    (32, 12, 2, [1500, 500], 10),
+])
+def test_coact_parity(E, k, L, counts, seed):
+    _say(f"coact E={E} k={k} L={L} counts={counts}")
+    off = synth.fam_offsets(counts)
+    tr = _rand_trace(L, int(off[-1]), k, E, seed)
+    D, C, err = tacg.coact_build(tr, off, E)
+    assert _err(err) == 0
+    Do, Co, eo = oracle.coact(tr.cpu(), off, E)
+    assert eo == 0
+    np.testing.assert_array_equal(_u32(D), Do)
+    np.testing.assert_array_equal(_u32(C), Co)
+
+
+def test_coact_tiny_config():
+    w = synth.make_workload("tiny", device="cuda")
+    D, C, err = tacg.coact_build(w.trace_group, w.fam_off_group, 8)
+    assert _err(err) == 0
+    Do, Co, _ = oracle.coact(w.trace_group.cpu(), w.fam_off_group, 8)
+    np.testing.assert_array_equal(_u32(D), Do)
+    np.testing.assert_array_equal(_u32(C), Co)
+
+
+def test_coact_accumulate_chunks():
+    """Streaming: counting a trace in two token chunks with TACG_ACCUMULATE equals one call."""
+    E, k = 64, 6
+    counts = [6000, 4000]
+    off = synth.fam_offsets(counts)
+    tr = _rand_trace(2, 10000, k, E, 11)
+    D, C, _ = tacg.coact_build(tr, off, E)
+    # chunk 1: first half of each family; chunk 2: second half (each chunk family-contiguous)
+    halves = []
+    for part in (0, 1):
+        idx, sub_counts = [], []
+        for f in range(2):
+            a, b = int(off[f]), int(off[f + 1])
+            mid = (a + b) // 2
+            lo, hi = (a, mid) if part == 0 else (mid, b)
+            idx.append(torch.arange(lo, hi))
+            sub_counts.append(hi - lo)
+        halves.append((tr[:, torch.cat(idx).cuda()].contiguous(), synth.fam_offsets(sub_counts)))
+    D2, C2, err = tacg.coact_build(halves[0][0], halves[0][1], E)
+    tacg.coact_build(halves[1][0], halves[1][1], E, D=D2, C=C2, accumulate=True, err=err)
+    assert _err(err) == 0
+    assert torch.equal(D, D2) and torch.equal(C, C2)
+
+
+def test_coact_repeat_is_deterministic():
+    E, k = 256, 8
+    tr = _rand_trace(3, 20000, k, E, 12)
+    off = [0, 12000, 20000]
+    D1, C1, _ = tacg.coact_build(tr, off, E)
+    D2, C2, _ = tacg.coact_build(tr, off, E)
+    assert torch.equal(D1, D2) and torch.equal(C1, C2)
+
+
+def test_coact_data_errors_flagged():
+    E, k = 16, 4
+    tr = _rand_trace(1, 3000, k, E, 13)
+    bad = tr.clone()
+    bad[0, 100, 1] = bad[0, 100, 0]
+    _, _, err = tacg.coact_build(bad, [0, 3000], E)
+    assert _err(err) & tacg.ERR_ID_DUP
+    bad = tr.clone()
+    bad[0, 7, 3] = E
+    _, _, err = tacg.coact_build(bad, [0, 3000], E)
+    assert _err(err) & tacg.ERR_ID_RANGE
+    bad = tr.clone()
+    bad[0, 9, 2] = -3
+    _, _, err = tacg.coact_build(bad, [0, 3000], E)
+    assert _err(err) & tacg.ERR_ID_RANGE
+
+
+def test_coact_empty_trace():
+    tr = torch.zeros((2, 0, 4), dtype=torch.int16, device="cuda")
+    D, C, err = tacg.coact_build(tr, [0, 0, 0], 16)
+    assert _err(err) == 0
+    assert int(D.abs().sum()) == 0 and int(C.abs().sum()) == 0
+
+
+# ------------------------------------------------------------------------------------------------
+# preferences and graph
+# ------------------------------------------------------------------------------------------------
+def _close(gpu, ref):
+    g = gpu.detach().cpu().double().numpy()
+    np.testing.assert_allclose(g, ref, rtol=RTOL, atol=ATOL)
+
+
+@pytest.mark.parametrize("name,alpha,tau", [("tiny", 0.25, 1.0), ("deepseek16b", 0.25, 1.0),
+                                            ("qwen15", 0.0, 0.5), ("qwen3_30b", 0.6, 2.0),
+                                            ("deepseek_v3", 0.25, 1.0)])
+def test_reweight_parity(name, alpha, tau):
+    cfg = synth.CONFIGS[name]
+    n = cfg.tokens_group if name == "tiny" else cfg.F * 3000
+    w = synth.make_workload(name, device="cuda", n_tokens=n, layers=min(cfg.L, 3))
+    _say(f"reweight {name}")
+    D, C, err = tacg.coact_build(w.trace_group, w.fam_off_group, cfg.E)
+    pref, at, ah = tacg.reweight(D, C, cfg.k, alpha=alpha, tau=tau, want_hat=True)
+    assert _err(err) == 0
+    Do, Co, _ = oracle.coact(w.trace_group.cpu(), w.fam_off_group, cfg.E)
+    po, ato, aho = oracle.reweight(Do, Co, cfg.k, alpha=alpha, tau=tau)
+    _close(pref, po)
+    _close(at, ato)
+    _close(ah, aho)
+
+
+def test_reweight_empty_family_and_zero_layer():
+    E, k = 12, 3
+    tr = _rand_trace(2, 900, k, E, 21)
+    off = [0, 500, 500, 900]                    # family 1 is empty
+    D, C, _ = tacg.coact_build(tr, off, E)
+    pref, at, ah = tacg.reweight(D, C, k, want_hat=True)
+    Do, Co, _ = oracle.coact(tr.cpu(), off, E)
+    po, ato, aho = oracle.reweight(Do, Co, k)
+    _close(pref, po)
+    _close(at, ato)
+    Dz = torch.zeros((3, 1, E), dtype=torch.int32, device="cuda")
+    Cz = torch.zeros((3, 1, E, E), dtype=torch.int32, device="cuda")
+    pref, at, ah = tacg.reweight(Dz, Cz, k, want_hat=True)
+    assert float(at.abs().max()) == 0.0 and float(ah.abs().max()) == 0.0
+    _close(pref, np.full((1, E, 3), 1 / 3))
+
+
+# ------------------------------------------------------------------------------------------------
+# placement scoring
+# ------------------------------------------------------------------------------------------------
+def _score_both(w, ps, E, theta=(3, 20), use_oracle_ref=False):
+    G = ps["n_gpus"]
+    prim = torch.as_tensor(ps["primary"]).cuda()
+    sec = torch.as_tensor(ps["secondary"]).cuda() if ps["secondary"] is not None else None
+    tr = w.trace_serve
+    Do, _, _ = oracle.coact(tr.cpu(), w.fam_off_serve, E)
+    ref_o = oracle.placement_load(Do, ps["primary"], G) if sec is not None else None
+    ref_g = None
+    if sec is not None:
+        if use_oracle_ref:
+            ref_g = torch.as_tensor(ref_o).cuda()
+        else:
+            D, _, e1 = tacg.coact_build(tr, w.fam_off_serve, E)
+            ref_g = tacg.placement_load(D, prim, G, err=e1)
+            assert _err(e1) == 0
+    out = tacg.eval_placements(tr, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, prim, sec, ref_g,
+                               theta=theta)
+    assert _err(out["err"]) == 0
+    ro = oracle.score(tr.cpu(), w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, ps["primary"],
+                      ps["secondary"], ref_o, theta)
+    assert ro["err"] == 0
+    if ref_g is not None:
+        np.testing.assert_array_equal(ref_g.cpu().numpy(), ref_o)
+    np.testing.assert_array_equal(out["cost_home"].cpu().numpy(), ro["cost_home"])
+    np.testing.assert_array_equal(out["cost_span"].cpu().numpy(), ro["cost_span"])
+    np.testing.assert_array_equal(_u32(out["load"]), ro["load"])
+    np.testing.assert_array_equal(out["cost_home_fam"].cpu().numpy(), ro["cost_home_fam"])
+    return out, ro
+
+
+@pytest.mark.parametrize("name,setidx,n_place,theta", [
+    ("tiny", 0, 16, (3, 20)),
+    ("deepseek16b", 0, 130, (3, 20)),
+    ("qwen15", 0, 70, (3, 20)),
+    ("qwen15", 1, 70, (0, 0)),
+    ("qwen3_30b", 0, 129, (3, 20)),
+    ("deepseek_v3", 0, 65, (3, 20)),
+    ("deepseek_v3", 0, 3, (0, 1)),
+])
+def test_eval_parity(name, setidx, n_place, theta):
+    cfg = synth.CONFIGS[name]
+    n = cfg.tokens_group if name == "tiny" else cfg.F * 1500 + 37
+    w = synth.make_workload(name, device="cuda", n_tokens=n, layers=min(cfg.L, 3), n_place=n_place)
+    _say(f"eval {name} set{setidx} P={n_place} theta={theta}")
+    _score_both(w, w.placement_sets[setidx], cfg.E, theta)
+
+
+def test_eval_with_oracle_snapshot():
+    cfg = synth.CONFIGS["deepseek_v3"]
+    w = synth.make_workload("deepseek_v3", device="cuda", n_tokens=16 * 800, layers=2, n_place=70)
+    _score_both(w, w.placement_sets[0], cfg.E, use_oracle_ref=True)
+
+
+def test_eval_home_only_and_single_gpu():
+    E, k, G, F = 8, 2, 4, 4
+    n = 300
+    tr = torch.zeros((2, F * n, k), dtype=torch.int16)
+    for f in range(F):
+        tr[:, f * n:(f + 1) * n, 0] = 2 * f
+        tr[:, f * n:(f + 1) * n, 1] = 2 * f + 1
+    tr = tr.cuda()
+    prim = torch.as_tensor((np.arange(E) // 2).astype(np.uint8)[None, None].repeat(2, axis=1)).cuda()
+    hs, hz = synth.home_bands(F, G)
+    out = tacg.eval_placements(tr, synth.fam_offsets([n] * F), E, hs, hz, G, prim)
+    assert _err(out["err"]) == 0
+    assert int(out["cost_home"][0]) == 0 and int(out["cost_span"][0]) == 0
+    prim1 = torch.zeros((3, 2, E), dtype=torch.uint8, device="cuda")
+    out = tacg.eval_placements(tr, synth.fam_offsets([n] * F), E, [0] * F, [1] * F, 1, prim1)
+    assert int(out["cost_home"].abs().sum()) == 0 and int(out["cost_span"].abs().sum()) == 0
+    assert np.all(_u32(out["load"]).sum(axis=2) == F * n * k)
+
+
+def test_eval_table_errors_flagged():
+    w = synth.make_workload("tiny", device="cuda")
+    ps = w.placement_sets[0]
+    prim = ps["primary"].copy()
+    prim[3, 1, 2] = 9
+    out = tacg.eval_placements(w.trace_serve, w.fam_off_serve, 8, ps["home_start"], ps["home_size"], 4,
+                               torch.as_tensor(prim).cuda())
+    assert _err(out["err"]) & tacg.ERR_TABLE
+
+
+def test_jain_parity():
+    rng = np.random.default_rng(5)
+    ld = rng.integers(0, 1 << 20, size=(37, 5, 32)).astype(np.int64)
+    ld[3] = 0
+    ld[4, :, 1:] = 0
+    t = torch.as_tensor(ld.astype(np.int32)).cuda()
+    j, v = tacg.jain_index(t)
+    jo, vo = oracle.jain(ld)
+    _close(j, jo)
+    _close(v, vo)
+    j, v = tacg.jain_index(t, per_layer=True)
+    jo, vo = oracle.jain(ld, per_layer=True)
+    _close(j, jo)
+    _close(v, vo)
