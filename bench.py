@@ -1,0 +1,227 @@
+#!/usr/bin/env python3
+"""Benchmark of the TACG/GESR trace passes on one MI355X.
+
+One step = one pass of the whole hot path over the resident synthetic input:
+  tacg_coact_build (grouping trace) -> tacg_reweight -> tacg_eval_placements (serving trace,
+  P placements with GESR replicas) -> tacg_jain.
+The placement tables and the snapshot loads that feed the guard are host inputs built before the
+timed region (the snapshot loads come from the serving trace's dispatch counts, computed with the
+same library before timing).
+
+Prints one JSON line.  Default workload: DeepSeek-V3-like shape (E=256, top-8, 58 MoE layers,
+16 families, 2^23 tokens per trace, 1024 placements on 32 simulated GPUs, 16 generic experts with 3
+secondaries each).  --config selects another preset.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "routed token·layers/sec (coact build) + placements×tokens/sec scored; % HBM BW"
+HBM_PEAK_GBS = 8000.0                 # MI355X HBM3E, GB/s
+N_CU, CLOCK_HZ = 256, 2.4e9
+VALU_PEAK_TOPS = N_CU * 64 * CLOCK_HZ / 1e12   # int32 lane-ops per second (64 lanes / CU / clock)
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", default="deepseek_v3")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=0, help="layers of the oracle's scoring sample (0 = all)")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; multi-GPU runs are not supported "
+                                   "(the simulated GPU count G is a parameter of the workload, not of the launch)"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2606_01007_amd as tacg
+    from paper_2606_01007_amd import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    dev = "cuda"
+    cfg = synth.CONFIGS[args.config]
+    t0 = time.time()
+    w = synth.make_workload(args.config, device=dev)
+    torch.cuda.synchronize()
+    gen_s = time.time() - t0
+    log(f"generated {args.config} in {gen_s:.1f} s")
+    ps = w.placement_sets[0]
+    E, k, L, F = cfg.E, cfg.k, cfg.L, cfg.F
+    G, P = ps["n_gpus"], ps["primary"].shape[0]
+    Ng, Ns = w.trace_group.shape[1], w.trace_serve.shape[1]
+    prim = torch.as_tensor(ps["primary"]).to(dev)
+    sec = torch.as_tensor(ps["secondary"]).to(dev) if ps["secondary"] is not None else None
+    theta = (3, 20)
+
+    # ---- host inputs, untimed: snapshot loads from the serving trace's dispatch counts ----
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ref = None
+    if sec is not None:
+        Ds, _, _ = tacg.coact_build(w.trace_serve, w.fam_off_serve, E, err=err)
+        ref = tacg.placement_load(Ds, prim, G, err=err)
+        del Ds
+
+    # ---- preallocated outputs and workspaces ----
+    D = torch.empty((F, L, E), dtype=torch.int32, device=dev)
+    C = torch.empty((F, L, E, E), dtype=torch.int32, device=dev)
+    ws_c = tacg.workspace(tacg.lib().tacg_coact_workspace_bytes(Ng, L, k, E, F), dev)
+    ws_r = tacg.workspace(tacg.lib().tacg_reweight_workspace_bytes(F, L, E), dev)
+    ws_e = tacg.workspace(tacg.lib().tacg_eval_workspace_bytes(Ns, L, E, G, P, F), dev)
+    out = dict(cost_home=torch.empty(P, dtype=torch.int64, device=dev),
+               cost_span=torch.empty(P, dtype=torch.int64, device=dev),
+               load=torch.empty((P, L, G), dtype=torch.int32, device=dev),
+               cost_home_fam=torch.empty((P, F), dtype=torch.int64, device=dev))
+
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+
+    def step(timed):
+        if timed:
+            ev[0].record()
+        tacg.coact_build(w.trace_group, w.fam_off_group, E, D=D, C=C, ws=ws_c, err=err)
+        if timed:
+            ev[1].record()
+        pref, at, _ = tacg.reweight(D, C, k, alpha=0.25, tau=1.0, eps=1e-8, ws=ws_r)
+        if timed:
+            ev[2].record()
+        tacg.eval_placements(w.trace_serve, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, prim, sec, ref,
+                             theta=theta, ws=ws_e, err=err, out=out)
+        if timed:
+            ev[3].record()
+        j, v = tacg.jain_index(out["load"])
+        if timed:
+            ev[4].record()
+        return j, v
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    log("warm-up done")
+    stage = np.zeros((args.steps, 4))
+    t_start = time.perf_counter()
+    for s in range(args.steps):
+        step(True)
+        torch.cuda.synchronize()
+        for i in range(4):
+            stage[s, i] = ev[i].elapsed_time(ev[i + 1]) * 1e-3
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    assert int(err.item()) == 0, f"device data error bits {int(err.item()):#x}"
+
+    t_coact, t_rw, t_eval, t_jain = stage.mean(axis=0)
+    tl = Ng * L                                        # routed token-layers per coact build
+    ptl = P * Ns * L                                   # placement-token-layers per scoring call
+    coact_rate = tl / t_coact
+    score_rate = P * Ns / t_eval                       # placements x tokens / s
+    trace_bytes_g = Ng * L * k * 2
+    trace_bytes_s = Ns * L * k * 2
+    c_bytes = F * L * E * E * 4 + F * L * E * 4
+    coact_gbs = (trace_bytes_g + c_bytes) / t_coact / 1e9
+    valu_ops = ptl * ((k - 1) + 3)                     # k-1 ORs of one-hot GPU masks, andn, 2 popcounts
+    eval_tops = valu_ops / t_eval / 1e12
+    result = {
+        "metric": METRIC,
+        "value": coact_rate,
+        "unit": "routed token·layers/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name}: E={E} top-{k} L={L} F={F}, grouping trace {Ng} tokens (uniform mix), "
+                        f"serving trace {Ns} tokens ({cfg.serve_mix} mix), {P} placements on G={G} cap "
+                        f"{ps['capacity']}, replicas {cfg.placements[0].n_generic_rep}x{cfg.placements[0].n_secondary}"
+                        f", theta=3/20",
+            "E": E, "top_k": k, "layers": L, "families": F, "tokens": Ng, "placements": P, "sim_gpus": G,
+        },
+        "coact_build": {"value": coact_rate, "unit": "routed token·layers/s", "ms": t_coact * 1e3,
+                        "hbm_GBps": coact_gbs, "hbm_frac": coact_gbs / HBM_PEAK_GBS},
+        "scoring": {"value": score_rate, "unit": "placements×tokens/s", "ms": t_eval * 1e3,
+                    "placement_token_layers_per_s": ptl / t_eval,
+                    "trace_equivalent_GBps": P * trace_bytes_s / t_eval / 1e9,
+                    "trace_equivalent_frac": P * trace_bytes_s / t_eval / 1e9 / HBM_PEAK_GBS},
+        "reweight_ms": t_rw * 1e3,
+        "jain_ms": t_jain * 1e3,
+        "roofline": {"kernel": "tacg_eval_placements (ev_main dominant)", "bound": "alu",
+                     "achieved": eval_tops, "peak": VALU_PEAK_TOPS, "unit": "TFLOP/s",
+                     "frac": eval_tops / VALU_PEAK_TOPS, "traffic": None,
+                     "note": "int32 lane-ops: (k-1) ORs + andn + 2 popcounts per placement-token-layer"},
+        "roofline_coact": {"kernel": "tacg_coact_build (coact_hist dominant)", "bound": "hbm",
+                           "achieved": coact_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": coact_gbs / HBM_PEAK_GBS, "traffic": None},
+        "gen_s": gen_s,
+    }
+
+    log(f"timed {args.steps} steps: {wall / args.steps * 1e3:.1f} ms/step")
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, ps, cfg, args.cpu_layers)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(w, ps, cfg, cpu_layers):
+    """The oracle as it stands, on this host's cores: the whole co-activation build of the grouping
+    trace, and one placement scored over the serving trace (scaled to placements x tokens / s)."""
+    import numpy as np
+    import oracle
+
+    oracle.build()
+    log("cpu baseline: oracle co-activation build")
+    tg = w.trace_group.cpu().numpy()
+    t0 = time.perf_counter()
+    _, _, e1 = oracle.coact(tg, w.fam_off_group, cfg.E)
+    t_coact = time.perf_counter() - t0
+    del tg
+    ts = w.trace_serve.cpu().numpy()
+    Ls = ts.shape[0] if cpu_layers <= 0 else min(cpu_layers, ts.shape[0])
+    ts = np.ascontiguousarray(ts[:Ls])
+    G = ps["n_gpus"]
+    sec = ps["secondary"][:, :Ls] if ps["secondary"] is not None else None
+    prim = ps["primary"][:, :Ls]
+    ref = None
+    if sec is not None:
+        Ds, _, _ = oracle.coact(ts, w.fam_off_serve, cfg.E)
+        ref = oracle.placement_load(Ds, prim, G)
+    log("cpu baseline: oracle scoring of one placement")
+    t0 = time.perf_counter()
+    r = oracle.score(ts, w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], G, prim, sec, ref, (3, 20),
+                     p_range=(0, 1))
+    t_score = time.perf_counter() - t0
+    Ns = ts.shape[1]
+    coact_rate = w.trace_group.shape[1] * w.trace_group.shape[0] / t_coact
+    return {"value": coact_rate, "unit": "routed token·layers/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"co-activation build of the whole grouping trace ({w.trace_group.shape[1]} tokens x "
+                      f"{w.trace_group.shape[0]} layers, {t_coact:.1f} s); scoring of placement 0 on the serving "
+                      f"trace over {Ls} layers ({t_score:.1f} s)",
+            "scoring_value": Ns * Ls / cfg.L / t_score if Ls else None,
+            "scoring_unit": "placements×tokens/s (one placement over all layers, scaled from the sample)",
+            "err": int(e1) | int(r["err"])}
+
+
+if __name__ == "__main__":
+    main()

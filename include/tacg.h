@@ -20,7 +20,7 @@
  * tokens [fam_off_host[f], fam_off_host[f+1]) with fam_off_host[0] = 0 and fam_off_host[F] = N.
  *
  * Limits: 1 <= E <= 256, 1 <= k <= min(E, 16), 1 <= F <= 64, 1 <= G <= 32 simulated GPUs,
- * 0 <= R <= 4 secondary GPUs per expert, at most 32 experts with secondaries per layer,
+ * 0 <= R <= 4 secondary GPUs per expert, at most 16 experts with secondaries per layer,
  * N * k < 2^32.
  */
 #ifndef TACG_H
@@ -54,7 +54,7 @@ extern "C" {
 #define TACG_MAX_FAMILIES 64
 #define TACG_MAX_GPUS 32
 #define TACG_MAX_SECONDARY 4
-#define TACG_MAX_REPLICATED 32
+#define TACG_MAX_REPLICATED 16
 
 /*
  * Dispatch and co-activation counts per task family and layer (Sec. 3.3, "Scoring task-family

@@ -4,12 +4,11 @@
 //
 // Launch sequence of tacg_eval_placements:
 //   ev_zero      clear the workspace accumulators
-//   ev_count     per-layer expert dispatch counts of the trace (and trace validation)
 //   ev_flags     validate the placement tables; mark experts that have a secondary in any placement
 //   ev_replist   per layer: compact index of the marked ("replicated") experts
 //   ev_repinfo   per (placement, layer, replicated expert): feasible candidate mask FC and the
 //                fallback GPU argmin_{m in FC} load_ref (ties: lowest number)
-//   ev_main      the trace pass (below)
+//   ev_main      the trace pass (below); also counts every expert's dispatches and validates ids
 //   ev_finalize  loads = counts of single-candidate experts on their primary + replicated choices;
 //                costs from the accumulators
 //
@@ -18,10 +17,9 @@
 //   * LDS holds, for the workgroup's placements and layer, the one-hot GPU mask of every expert
 //     (tbl[e][p], uint32; zero for replicated experts), the replica info (FC, fallback) and
 //     per-placement counters of the GPUs chosen for replicated experts.
-//   * A wave loads 64 token-layers at once (one coalesced load per lane), turns each id into the LDS
-//     byte offset of its table row (packed two per dword) and builds a per-token word with the
-//     replicated-slot mask and the anchor GPU; the per-token loop then broadcasts them with
-//     v_readlane, so the row offsets live in SGPRs.
+//   * A wave loads 64 token-layers at once (one load per lane), packs the expert ids four per dword
+//     and builds a per-token word with the replicated-slot mask, the anchor GPU and the replica
+//     indices; the per-token loop broadcasts them with v_readlane, so the ids live in SGPRs.
 //   * Per token-layer and lane: k conflict-free LDS reads (64 consecutive dwords per wave), OR of the
 //     masks, then (rarely) the replicated slots, then two popcounts into per-lane accumulators.
 #include "tacg_internal.h"
@@ -30,7 +28,7 @@ namespace tacg {
 namespace {
 
 constexpr int kMainThreads = 1024;
-constexpr int kMaxPieces = 256;
+constexpr int kMaxPieces = 160;
 constexpr uint8_t kNone = 0xFF;
 
 struct EvWs {
@@ -74,12 +72,13 @@ struct EvArgs {
   int32_t L, K, E, F, G, P, R;
   int32_t theta_num, theta_den;
   int32_t n_pieces;
-  uint32_t fam_off[TACG_MAX_FAMILIES + 1];
-  uint8_t home_start[TACG_MAX_FAMILIES];
-  uint8_t home_size[TACG_MAX_FAMILIES];
-  uint32_t piece_begin[kMaxPieces + 1];  // token ranges [piece_begin[j], piece_begin[j+1]) in one family
-  uint8_t piece_fam[kMaxPieces];
+  // One record per piece of one family's tokens: (first token, end token, family offset,
+  // home_start | home_size << 8 | family << 16).  Kept as 16-byte records: indexing kernel-argument
+  // arrays of different element sizes with one runtime index lets the compiler fold the byte and
+  // dword offsets into an unaligned scalar-load base, which the scalar unit does not honour.
+  uint4 piece[kMaxPieces];
 };
+static_assert(sizeof(EvArgs) <= 4096, "kernel arguments must stay within 4 KB");
 
 // ------------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void ev_zero(EvArgs a) {
@@ -96,46 +95,12 @@ __global__ __launch_bounds__(256) void ev_zero(EvArgs a) {
   for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.L * a.G; j += stride) w.rep_load[j] = 0;
 }
 
-// Expert dispatch counts per layer; validates ids (range, repeats).  grid (splits, L).
-__global__ __launch_bounds__(256) void ev_count(EvArgs a) {
-  __shared__ uint32_t h[TACG_MAX_EXPERTS];
-  const int l = blockIdx.y;
-  for (int i = threadIdx.x; i < a.E; i += blockDim.x) h[i] = 0;
-  __syncthreads();
-  const int64_t n = a.N;
-  const int64_t t0 = n * blockIdx.x / gridDim.x, t1 = n * (blockIdx.x + 1) / gridDim.x;
-  uint32_t err = 0;
-  for (int64_t t = t0 + threadIdx.x; t < t1; t += blockDim.x) {
-    const int16_t* ids = a.trace + (static_cast<int64_t>(l) * n + t) * a.K;
-    int v[TACG_MAX_TOPK];
-    bool ok = true;
-    for (int s = 0; s < a.K; ++s) {
-      v[s] = ids[s];
-      if (v[s] < 0 || v[s] >= a.E) {
-        err |= TACG_ERR_ID_RANGE;
-        ok = false;
-      }
-      for (int q = 0; q < s; ++q)
-        if (v[q] == v[s]) {
-          err |= TACG_ERR_ID_DUP;
-          ok = false;
-        }
-    }
-    if (ok)
-      for (int s = 0; s < a.K; ++s) atomicAdd(&h[v[s]], 1u);
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < a.E; i += blockDim.x)
-    if (h[i]) atomicAdd(&a.ws.cnt[static_cast<int64_t>(l) * a.E + i], h[i]);
-  if (err) atomicOr(a.d_err, err);
-}
-
-// Table validation and the replicated-expert marks.  grid (P, L), one thread per expert.
+// Table validation and the replicated-expert marks.  Flat grid-stride loop over (p, l, e).
 __global__ __launch_bounds__(256) void ev_flags(EvArgs a) {
-  const int p = blockIdx.x, l = blockIdx.y;
+  const int64_t n = static_cast<int64_t>(a.P) * a.L * a.E;
   uint32_t err = 0;
-  for (int e = threadIdx.x; e < a.E; e += blockDim.x) {
-    const int64_t pe = (static_cast<int64_t>(p) * a.L + l) * a.E + e;
+  for (int64_t pe = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; pe < n;
+       pe += static_cast<int64_t>(gridDim.x) * blockDim.x) {
     const uint8_t g0 = a.primary[pe];
     if (g0 >= a.G) err |= TACG_ERR_TABLE;
     bool any = false;
@@ -150,7 +115,11 @@ __global__ __launch_bounds__(256) void ev_flags(EvArgs a) {
       seen |= 1u << g;
       any = true;
     }
-    if (any) atomicOr(&a.ws.flagbits[l * 8 + (e >> 5)], 1u << (e & 31));
+    if (any) {
+      const int e = static_cast<int>(pe % a.E);
+      const int l = static_cast<int>((pe / a.E) % a.L);
+      atomicOr(&a.ws.flagbits[l * 8 + (e >> 5)], 1u << (e & 31));
+    }
   }
   if (err) atomicOr(a.d_err, err);
 }
@@ -225,21 +194,269 @@ __global__ __launch_bounds__(256) void ev_repinfo(EvArgs a) {
 }
 
 // ------------------------------------------------------------------------------------------------
-// The trace pass.  PPL placements per lane; workgroup = 64 * PPL placements of one layer and one
-// piece of one family's tokens.  grid (placement blocks, pieces, L).
+// The trace pass.  PPL placements per lane (one 8- or 16-byte LDS read per slot serves all of them);
+// a workgroup scores 64 * PPL placements of one layer on one piece of one family's tokens.
+// grid (placement blocks, pieces, L).  The workgroups of placement block 0 also count the
+// dispatches of every expert and validate the ids (each token-layer is seen by exactly one of them).
+// Choices for replicated experts are counted in 16-bit LDS counters (two per dword), flushed to the
+// workspace after every round of at most 65535 / K tokens so that they cannot overflow.
+//
+// Per-token word `info` built by the lane that loaded the token-layer (wave-uniform after v_readlane):
+//   K <= 8:  bits 0-7 replicated-slot mask, 8-12 band position of the anchor GPU within its family's
+//            band, then 4-bit replica indices of the first four replicated slots (13-16 ... 25-28);
+//   K > 8:   bits 0-15 replicated-slot mask, 16-20 band position, replica indices of the first two
+//            replicated slots (21-24, 25-28).
+// Further replicated slots of a token look their index up in LDS.
+template <int K>
+struct InfoLayout {
+  static constexpr int kMaskBits = K <= 8 ? 8 : 16;
+  static constexpr int kHomeShift = kMaskBits;
+  static constexpr int kRepShift = kMaskBits + 5;
+  static constexpr int kRepSlots = K <= 8 ? 4 : 2;
+};
+
+// Index of the lowest set bit, 0xffffffff for 0 (the hardware v_ffbl_b32 result).
+__device__ __forceinline__ uint32_t find_first_bit(uint32_t x) {
+  uint32_t r;
+  asm("v_ffbl_b32 %0, %1" : "=v"(r) : "v"(x));
+  return r;
+}
+
+template <int K, int PPL, bool NARROW>
+struct Scorer {
+  static constexpr int PW = 64 * PPL;
+  static constexpr int KB = (K + 3) / 4;  // dwords of 8-bit expert ids per token-layer
+  static constexpr int kRowShift = PPL == 2 ? 9 : 10;  // log2 of a table row in bytes (PW * 4)
+  using IL = InfoLayout<K>;
+
+  const char* tbl_lane;   // LDS table base + this lane's column offset
+  const uint2* rinfo;     // [MAX_REP][PW]
+  uint32_t* rcnt;         // [G][PW / 2]
+  const uint8_t* rep_of;  // [E]
+  int lane;
+  uint32_t acc_span[PPL], acc_home[PPL];
+
+  // one-hot GPU masks of the token's single-candidate experts, OR-ed per placement
+  __device__ __forceinline__ void gather(const uint32_t (&ids)[KB], uint32_t (&m)[PPL]) const {
+#pragma unroll
+    for (int q = 0; q < PPL; ++q) m[q] = 0;
+#pragma unroll
+    for (int s = 0; s < K; ++s) {
+      const uint32_t id = __builtin_amdgcn_ubfe(ids[s >> 2], 8 * (s & 3), 8);
+      const char* base = tbl_lane + (id << kRowShift);
+      if constexpr (PPL == 2) {
+        const uint2 v = *reinterpret_cast<const uint2*>(base);
+        m[0] |= v.x;
+        m[1] |= v.y;
+      } else {
+        const uint4 v = *reinterpret_cast<const uint4*>(base);
+        m[0] |= v.x;
+        m[1] |= v.y;
+        m[2] |= v.z;
+        m[3] |= v.w;
+      }
+    }
+  }
+
+  // Replicated slots in slot order: the lowest-numbered feasible candidate the token already
+  // reaches, else the anchor if it is a feasible candidate, else the least-loaded feasible candidate.
+  // rinfo[r][p] = (FC mask, packed fallbacks): byte i holds 32 + (the choice when no candidate is
+  // reached) for the anchor at band position i (bands of up to 4 GPUs; wider bands keep 32 + the
+  // least-loaded feasible candidate and test the anchor here).  ffbl(0) = 0xffffffff, so min(ffbl(x), 32 + fb)
+  // selects the reached candidate when there is one; the shift and the counter row use its low 5 bits.
+  __device__ __forceinline__ void resolve(uint32_t info, const uint32_t (&ids)[KB], uint32_t (&m)[PPL]) {
+    const uint32_t repmask = info & ((1u << IL::kMaskBits) - 1u);
+    if (!repmask) return;
+    const uint32_t hshift = 8u * ((info >> IL::kHomeShift) & 31u);  // 8 * band position of the anchor
+    int nth = 0;
+#pragma unroll
+    for (int s = 0; s < K; ++s) {
+      if (!((repmask >> s) & 1u)) continue;
+      uint32_t r;
+      if (nth < IL::kRepSlots) {
+        r = (info >> (IL::kRepShift + 4 * nth)) & 15u;
+      } else {
+        r = rep_of[__builtin_amdgcn_ubfe(ids[s >> 2], 8 * (s & 3), 8)];
+      }
+      ++nth;
+      const uint2* rp = rinfo + r * PW + lane * PPL;
+      uint2 ri[PPL];
+#pragma unroll
+      for (int q = 0; q < PPL; q += 2) {
+        const uint4 v = *reinterpret_cast<const uint4*>(rp + q);
+        ri[q] = make_uint2(v.x, v.y);
+        ri[q + 1] = make_uint2(v.z, v.w);
+      }
+#pragma unroll
+      for (int q = 0; q < PPL; ++q) {
+        const uint32_t x = ri[q].x & m[q];
+        uint32_t fb;
+        if constexpr (NARROW) {
+          fb = __builtin_amdgcn_ubfe(ri[q].y, hshift, 8);
+        } else {
+          const uint32_t h = home_start + (hshift >> 3);
+          fb = ((ri[q].x >> h) & 1u) ? 32u + h : ri[q].y;
+        }
+        const uint32_t pick = min(find_first_bit(x), fb) & 31u;
+        m[q] |= 1u << pick;
+        __hip_atomic_fetch_add(&rcnt[(pick * PW + lane * PPL + q) >> 1], 1u << (16 * (q & 1)), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+    }
+  }
+
+  uint32_t home_start;
+
+  __device__ __forceinline__ void account(uint32_t info, const uint32_t (&m)[PPL]) {
+    const uint32_t not_h = ~(1u << (home_start + ((info >> IL::kHomeShift) & 31u)));
+#pragma unroll
+    for (int q = 0; q < PPL; ++q) {
+      acc_span[q] += __popc(m[q]);
+      acc_home[q] += __popc(m[q] & not_h);
+    }
+  }
+};
+
+// Token loop of one workgroup (see ev_main).  NARROW: the family's band has at most 4 GPUs, so the
+// fallback choices are packed per band position.
+template <int K, int PPL, bool NARROW>
+__device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl, const uint2* rinfo, uint32_t* rcnt,
+                                            uint32_t* ecnt, const uint8_t* rep_of, int l, int p0, int nrep,
+                                            bool counter, uint32_t t_begin, uint32_t t_end, uint32_t off_f,
+                                            uint32_t hs, uint32_t hz, uint32_t& err, uint32_t (&acc_span)[PPL],
+                                            uint32_t (&acc_home)[PPL]) {
+  using S = Scorer<K, PPL, NARROW>;
+  using IL = InfoLayout<K>;
+  constexpr int PW = S::PW;
+  constexpr int KB = S::KB;
+  constexpr int U = 4;             // token-layers scored together (independent LDS reads in flight)
+  constexpr uint32_t round_tokens = 65535u / K;
+  const int E = a.E, G = a.G, L = a.L;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int nwaves = blockDim.x >> 6;
+  const int16_t* trace_l = a.trace + static_cast<int64_t>(l) * a.N * K;
+  S sc;
+  sc.tbl_lane = reinterpret_cast<const char*>(tbl) + lane * PPL * 4;
+  sc.rinfo = rinfo;
+  sc.rcnt = rcnt;
+  sc.rep_of = rep_of;
+  sc.lane = lane;
+  sc.home_start = hs;
+#pragma unroll
+  for (int q = 0; q < PPL; ++q) sc.acc_span[q] = sc.acc_home[q] = 0;
+
+  for (uint32_t r_begin = t_begin; r_begin < t_end; r_begin += round_tokens) {
+    const uint32_t r_end = min(t_end, r_begin + round_tokens);
+    for (uint32_t tile = r_begin + wave * 64u; tile < r_end; tile += nwaves * 64u) {
+      // ---- per-lane preprocessing of token-layer (tile + lane) ----
+      const uint32_t t = tile + lane;
+      uint32_t pk[KB];
+#pragma unroll
+      for (int w = 0; w < KB; ++w) pk[w] = 0;
+      uint32_t info = 0;
+      if (t < r_end) {
+        const int16_t* idp = trace_l + static_cast<int64_t>(t) * K;
+        uint32_t raw[K];
+#pragma unroll
+        for (int s = 0; s < K; ++s) raw[s] = static_cast<uint16_t>(idp[s]);
+        bool ok = true;
+        int nth = 0;
+#pragma unroll
+        for (int s = 0; s < K; ++s) {
+          const uint32_t id = min(raw[s], static_cast<uint32_t>(E - 1));
+          ok &= raw[s] < static_cast<uint32_t>(E);
+          const uint32_t r = rep_of[id];
+          if (r != kNone) {
+            info |= 1u << s;
+            if (nth < IL::kRepSlots) info |= r << (IL::kRepShift + 4 * nth);
+            ++nth;
+          }
+          pk[s >> 2] |= id << (8 * (s & 3));
+        }
+        info |= ((t - off_f) % hz) << IL::kHomeShift;
+        if (counter) {
+          bool dup = false;
+#pragma unroll
+          for (int s = 1; s < K; ++s)
+#pragma unroll
+            for (int q = 0; q < s; ++q) dup |= raw[s] == raw[q];
+          if (!ok) err |= TACG_ERR_ID_RANGE;
+          if (dup) err |= TACG_ERR_ID_DUP;
+          if (ok && !dup) {
+#pragma unroll
+            for (int s = 0; s < K; ++s)
+              __hip_atomic_fetch_add(&ecnt[raw[s]], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          }
+        }
+      }
+      const uint32_t ntile = min(64u, r_end - tile);
+      uint32_t j = 0;
+      for (; j + U <= ntile; j += U) {
+        uint32_t ids[U][KB], tinfo[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+          for (int w = 0; w < KB; ++w) ids[u][w] = __builtin_amdgcn_readlane(pk[w], j + u);
+          tinfo[u] = __builtin_amdgcn_readlane(info, j + u);
+        }
+        uint32_t m[U][PPL];
+#pragma unroll
+        for (int u = 0; u < U; ++u) sc.gather(ids[u], m[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          sc.resolve(tinfo[u], ids[u], m[u]);
+          sc.account(tinfo[u], m[u]);
+        }
+      }
+      for (; j < ntile; ++j) {
+        uint32_t ids[KB];
+#pragma unroll
+        for (int w = 0; w < KB; ++w) ids[w] = __builtin_amdgcn_readlane(pk[w], j);
+        const uint32_t tinfo = __builtin_amdgcn_readlane(info, j);
+        uint32_t m[PPL];
+        sc.gather(ids, m);
+        sc.resolve(tinfo, ids, m);
+        sc.account(tinfo, m);
+      }
+    }
+    if (nrep > 0) {  // flush the 16-bit choice counters of this round (nrep is workgroup-uniform)
+      __syncthreads();
+      for (int i = threadIdx.x; i < G * PW / 2; i += blockDim.x) {
+        const uint32_t v = rcnt[i];
+        if (v) {
+          const int g = (2 * i) / PW, q = 2 * i - g * PW, p = p0 + q;
+          uint32_t* dst = a.ws.rep_load + (static_cast<int64_t>(p) * L + l) * G + g;
+          if (p < a.P && (v & 0xffffu)) atomicAdd(dst, v & 0xffffu);
+          if (p + 1 < a.P && (v >> 16)) atomicAdd(dst + static_cast<int64_t>(L) * G, v >> 16);
+          rcnt[i] = 0;
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+#pragma unroll
+  for (int q = 0; q < PPL; ++q) {
+    acc_span[q] = sc.acc_span[q];
+    acc_home[q] = sc.acc_home[q];
+  }
+}
+
 template <int K, int PPL>
 __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
   extern __shared__ __align__(16) uint32_t lds[];
   constexpr int PW = 64 * PPL;
-  constexpr int KW = (K + 1) / 2;  // dwords of packed row offsets per token-layer
   const int E = a.E, G = a.G, L = a.L;
   const int pb = blockIdx.x, piece = blockIdx.y, l = blockIdx.z;
   const int p0 = pb * PW;
   const int nrep = a.ws.n_rep[l];
-  uint32_t* tbl = lds;                                                // [E][PW]
-  uint2* rinfo = reinterpret_cast<uint2*>(lds + E * PW);              // [MAX_REP][PW]
-  uint32_t* rcnt = lds + E * PW + 2 * TACG_MAX_REPLICATED * PW;       // [G][PW]
-  uint8_t* rep_of = reinterpret_cast<uint8_t*>(rcnt + G * PW);        // [E]
+  const bool counter = (pb == 0);
+  uint32_t* tbl = lds;                                                // [E][PW] one-hot GPU masks
+  uint2* rinfo = reinterpret_cast<uint2*>(lds + E * PW);              // [MAX_REP][PW] (FC, fallback)
+  uint32_t* rcnt = lds + E * PW + 2 * TACG_MAX_REPLICATED * PW;       // [G][PW / 2] two u16 counters
+  uint32_t* ecnt = rcnt + G * PW / 2;                                 // [E] dispatch counts
+  uint8_t* rep_of = reinterpret_cast<uint8_t*>(ecnt + E);             // [E]
   const uint8_t* rep_of_g = a.ws.rep_of + static_cast<int64_t>(l) * E;
 
   for (int i = threadIdx.x; i < E * PW; i += blockDim.x) {
@@ -251,104 +468,43 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
     }
     tbl[i] = v;
   }
-  for (int i = threadIdx.x; i < nrep * PW; i += blockDim.x) {
-    const int r = i / PW, q = i - r * PW, p = p0 + q;
-    rinfo[i] = p < a.P ? a.ws.rep_info[(static_cast<int64_t>(l) * TACG_MAX_REPLICATED + r) * a.P + p]
-                       : make_uint2(1u, 0u);
+  const uint4 pc = a.piece[piece];
+  const uint32_t t_begin = pc.x, t_end = pc.y, off_f = pc.z;
+  const uint32_t hs = pc.w & 0xffu, hz = (pc.w >> 8) & 0xffu;
+  const int f = static_cast<int>(pc.w >> 16);
+  {
+    for (int i = threadIdx.x; i < nrep * PW; i += blockDim.x) {
+      const int r = i / PW, q = i - r * PW, p = p0 + q;
+      uint2 v = make_uint2(1u, 0u);
+      if (p < a.P) v = a.ws.rep_info[(static_cast<int64_t>(l) * TACG_MAX_REPLICATED + r) * a.P + p];
+      uint32_t pack = 32u + v.y;  // bands wider than 4 GPUs: the plain fallback (+32)
+      if (hz <= 4) {
+        pack = 0;
+        for (uint32_t b = 0; b < hz; ++b) {
+          const uint32_t h = hs + b;
+          pack |= (32u + (((v.x >> h) & 1u) ? h : v.y)) << (8 * b);
+        }
+      }
+      rinfo[i] = make_uint2(v.x, pack);
+    }
   }
-  for (int i = threadIdx.x; i < G * PW; i += blockDim.x) rcnt[i] = 0;
-  for (int i = threadIdx.x; i < E; i += blockDim.x) rep_of[i] = rep_of_g[i];
+  for (int i = threadIdx.x; i < G * PW / 2; i += blockDim.x) rcnt[i] = 0;
+  for (int i = threadIdx.x; i < E; i += blockDim.x) {
+    rep_of[i] = rep_of_g[i];
+    ecnt[i] = 0;
+  }
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nwaves = blockDim.x >> 6;
-  const int f = a.piece_fam[piece];
-  const uint32_t t_begin = a.piece_begin[piece], t_end = a.piece_begin[piece + 1];
-  const uint32_t off_f = a.fam_off[f];
-  const uint32_t hs = a.home_start[f], hz = a.home_size[f];
-  const uint32_t lane_off = static_cast<uint32_t>(lane) * PPL * 4u;
-  constexpr uint32_t row_bytes = PW * 4u;
-  const int16_t* trace_l = a.trace + static_cast<int64_t>(l) * a.N * K;
+  uint32_t err = 0;
 
   uint32_t acc_span[PPL], acc_home[PPL];
-#pragma unroll
-  for (int q = 0; q < PPL; ++q) acc_span[q] = acc_home[q] = 0;
-
-  for (uint32_t tile = t_begin + wave * 64u; tile < t_end; tile += nwaves * 64u) {
-    // ---- per-lane preprocessing of token-layer (tile + lane) ----
-    const uint32_t t = tile + lane;
-    uint32_t packed[KW];
-    uint32_t info = 0;  // bits 0..15 replicated-slot mask, bits 16..20 anchor GPU
-    if (t < t_end) {
-      const int16_t* ids = trace_l + static_cast<int64_t>(t) * K;
-#pragma unroll
-      for (int w = 0; w < KW; ++w) packed[w] = 0;
-#pragma unroll
-      for (int s = 0; s < K; ++s) {
-        uint32_t id = static_cast<uint16_t>(ids[s]);
-        id = min(id, static_cast<uint32_t>(E - 1));
-        if (rep_of[id] != kNone) info |= 1u << s;
-        packed[s >> 1] |= (id * row_bytes) << (16 * (s & 1));
-      }
-      info |= (hs + (t - off_f) % hz) << 16;
-    } else {
-#pragma unroll
-      for (int w = 0; w < KW; ++w) packed[w] = 0;
-    }
-    const uint32_t ntile = min(64u, t_end - tile);
-    for (uint32_t j = 0; j < ntile; ++j) {
-      uint32_t rows[KW];
-#pragma unroll
-      for (int w = 0; w < KW; ++w) rows[w] = __builtin_amdgcn_readlane(packed[w], j);
-      const uint32_t tinfo = __builtin_amdgcn_readlane(info, j);
-      uint32_t m[PPL];
-#pragma unroll
-      for (int q = 0; q < PPL; ++q) m[q] = 0;
-#pragma unroll
-      for (int s = 0; s < K; ++s) {
-        const uint32_t row = (s & 1) ? (rows[s >> 1] >> 16) : (rows[s >> 1] & 0xffffu);
-        const char* base = reinterpret_cast<const char*>(tbl) + row + lane_off;
-        if constexpr (PPL == 1) {
-          m[0] |= *reinterpret_cast<const uint32_t*>(base);
-        } else if constexpr (PPL == 2) {
-          const uint2 v = *reinterpret_cast<const uint2*>(base);
-          m[0] |= v.x;
-          m[1] |= v.y;
-        } else {
-          const uint4 v = *reinterpret_cast<const uint4*>(base);
-          m[0] |= v.x;
-          m[1] |= v.y;
-          m[2] |= v.z;
-          m[3] |= v.w;
-        }
-      }
-      const uint32_t h = tinfo >> 16;
-      uint32_t repmask = tinfo & 0xffffu;
-      while (repmask) {  // replicated slots, in slot order (wave-uniform)
-        const int s = __builtin_ctz(repmask);
-        repmask &= repmask - 1u;
-        const uint32_t row = (s & 1) ? (rows[s >> 1] >> 16) : (rows[s >> 1] & 0xffffu);
-        const uint32_t id = row / row_bytes;
-        const int r = rep_of[id];
-#pragma unroll
-        for (int q = 0; q < PPL; ++q) {
-          const uint2 ri = rinfo[r * PW + lane * PPL + q];
-          const uint32_t x = ri.x & m[q];
-          const uint32_t fb = ((ri.x >> h) & 1u) ? h : ri.y;
-          const uint32_t pick = x ? static_cast<uint32_t>(__builtin_ctz(x)) : fb;
-          m[q] |= 1u << pick;
-          __hip_atomic_fetch_add(&rcnt[pick * PW + lane * PPL + q], 1u, __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_WORKGROUP);
-        }
-      }
-      const uint32_t not_h = ~(1u << h);
-#pragma unroll
-      for (int q = 0; q < PPL; ++q) {
-        acc_span[q] += __popc(m[q]);
-        acc_home[q] += __popc(m[q] & not_h);
-      }
-    }
+  if (hz <= 4) {
+    score_piece<K, PPL, true>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end, off_f, hs, hz,
+                              err, acc_span, acc_home);
+  } else {
+    score_piece<K, PPL, false>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end, off_f, hs, hz,
+                               err, acc_span, acc_home);
   }
 
   // ---- flush ----
@@ -363,12 +519,11 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
       }
     }
   }
-  __syncthreads();
-  if (nrep > 0) {
-    for (int i = threadIdx.x; i < G * PW; i += blockDim.x) {
-      const int g = i / PW, q = i - g * PW, p = p0 + q;
-      if (p < a.P && rcnt[i]) atomicAdd(&a.ws.rep_load[(static_cast<int64_t>(p) * L + l) * G + g], rcnt[i]);
-    }
+  if (err) atomicOr(a.d_err, err);
+  if (counter) {
+    __syncthreads();
+    for (int i = threadIdx.x; i < E; i += blockDim.x)
+      if (ecnt[i]) atomicAdd(&a.ws.cnt[static_cast<int64_t>(l) * E + i], ecnt[i]);
   }
 }
 
@@ -407,7 +562,7 @@ template <int K, int PPL>
 int launch_main(const EvArgs& a, int n_pblocks, hipStream_t stream) {
   constexpr int PW = 64 * PPL;
   const size_t lds = static_cast<size_t>(a.E) * PW * 4 + static_cast<size_t>(2) * TACG_MAX_REPLICATED * PW * 4 +
-                     static_cast<size_t>(a.G) * PW * 4 + align256(a.E);
+                     static_cast<size_t>(a.G) * PW * 2 + static_cast<size_t>(a.E) * 4 + align256(a.E);
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&ev_main<K, PPL>), hipFuncAttributeMaxDynamicSharedMemorySize,
                       static_cast<int>(lds));
   hipLaunchKernelGGL((ev_main<K, PPL>), dim3(n_pblocks, a.n_pieces, a.L), dim3(kMainThreads), lds, stream, a);
@@ -416,8 +571,8 @@ int launch_main(const EvArgs& a, int n_pblocks, hipStream_t stream) {
 
 template <int K>
 int launch_main_k(const EvArgs& a, hipStream_t stream) {
-  if (a.E > 128) return launch_main<K, 1>(a, (a.P + 63) / 64, stream);
-  return launch_main<K, 2>(a, (a.P + 127) / 128, stream);
+  if (a.E > 64) return launch_main<K, 2>(a, (a.P + 127) / 128, stream);
+  return launch_main<K, 4>(a, (a.P + 255) / 256, stream);
 }
 
 // per-(placement, layer) primary-only loads from D.  grid (P, L), 256 threads.
@@ -511,11 +666,6 @@ int launch_eval(const int16_t* trace, int64_t N, int32_t L, int32_t K, int32_t E
   a.R = R;
   a.theta_num = theta_num;
   a.theta_den = theta_den;
-  for (int f = 0; f <= F; ++f) a.fam_off[f] = static_cast<uint32_t>(fam_off_host[f]);
-  for (int f = 0; f < F; ++f) {
-    a.home_start[f] = static_cast<uint8_t>(home_start_host[f]);
-    a.home_size[f] = static_cast<uint8_t>(home_size_host[f]);
-  }
   // pieces: split every family's tokens into chunks of about N / 64 tokens (at least 4096, at
   // most 2^26 so that the per-lane 32-bit cost accumulators cannot overflow)
   int64_t chunk = std::min<int64_t>(int64_t(1) << 26, std::max<int64_t>(4096, (N + 63) / 64));
@@ -533,21 +683,23 @@ int launch_eval(const int16_t* trace, int64_t N, int32_t L, int32_t K, int32_t E
   np = 0;
   for (int f = 0; f < F; ++f) {
     for (int64_t t = fam_off_host[f]; t < fam_off_host[f + 1]; t += chunk) {
-      a.piece_begin[np] = static_cast<uint32_t>(t);
-      a.piece_fam[np] = static_cast<uint8_t>(f);
+      const int64_t e = std::min<int64_t>(t + chunk, fam_off_host[f + 1]);
+      a.piece[np] = make_uint4(static_cast<uint32_t>(t), static_cast<uint32_t>(e),
+                               static_cast<uint32_t>(fam_off_host[f]),
+                               static_cast<uint32_t>(home_start_host[f]) |
+                                   (static_cast<uint32_t>(home_size_host[f]) << 8) |
+                                   (static_cast<uint32_t>(f) << 16));
       ++np;
     }
   }
   a.n_pieces = np;
-  // families are contiguous in token order, so piece j always ends where piece j + 1 begins
-  a.piece_begin[np] = static_cast<uint32_t>(N);
 
   hipLaunchKernelGGL(ev_zero, dim3(256), dim3(256), 0, stream, a);
-  if (N > 0) {
-    const int splits = static_cast<int>(std::min<int64_t>(64, (N + 65535) / 65536));
-    hipLaunchKernelGGL(ev_count, dim3(splits, L), dim3(256), 0, stream, a);
+  {
+    const int64_t n = static_cast<int64_t>(P) * L * E;
+    const int blocks = static_cast<int>(std::min<int64_t>(2048, (n + 255) / 256));
+    hipLaunchKernelGGL(ev_flags, dim3(blocks), dim3(256), 0, stream, a);
   }
-  hipLaunchKernelGGL(ev_flags, dim3(P, L), dim3(256), 0, stream, a);
   hipLaunchKernelGGL(ev_replist, dim3(L), dim3(256), 0, stream, a);
   if (R > 0) hipLaunchKernelGGL(ev_repinfo, dim3((P + 255) / 256, L), dim3(256), 0, stream, a);
   if (hipGetLastError() != hipSuccess) return TACG_E_DEVICE;

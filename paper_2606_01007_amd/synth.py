@@ -256,18 +256,20 @@ def random_placements(P: int, L: int, E: int, G: int, cap: int, seed: int,
 
 def random_secondaries(primary: np.ndarray, G: int, rep_experts: np.ndarray, n_sec: int,
                        seed: int) -> np.ndarray:
-    """For each (p, l) and each expert of rep_experts[l], n_sec distinct GPUs != its primary.
-    Other experts get 0xFF (no secondary)."""
+    """For each (p, l) and each expert of rep_experts[l], n_sec distinct random GPUs other than its
+    primary.  Other experts get 0xFF (no secondary)."""
     P, L, E = primary.shape
-    sec = np.full((P, L, E, max(n_sec, 1)), NONE, dtype=np.uint8)
     if n_sec == 0:
-        return sec[..., :0]
+        return np.full((P, L, E, 0), NONE, dtype=np.uint8)
+    sec = np.full((P, L, E, n_sec), NONE, dtype=np.uint8)
     rng = np.random.default_rng(seed)
-    for p in range(P):
-        for l in range(L):
-            for e in rep_experts[l]:
-                choices = np.array([g for g in range(G) if g != primary[p, l, e]], dtype=np.uint8)
-                sec[p, l, e] = rng.choice(choices, size=n_sec, replace=False)
+    R = rep_experts.shape[1]
+    lidx = np.arange(L)[:, None]
+    prim_rep = primary[:, lidx, rep_experts]                     # [P][L][R]
+    keys = rng.random((P, L, R, G))
+    np.put_along_axis(keys, prim_rep[..., None].astype(np.int64), np.inf, axis=3)
+    pick = np.argsort(keys, axis=3, kind="stable")[..., :n_sec].astype(np.uint8)
+    sec[:, lidx, rep_experts] = pick
     return sec
 
 

@@ -236,6 +236,18 @@ def test_eval_parity(name, setidx, n_place, theta):
     _score_both(w, w.placement_sets[setidx], cfg.E, theta)
 
 
+@pytest.mark.parametrize("band", [1, 2, 4, 8])
+def test_eval_band_widths(band):
+    """Anchor bands of 1, 2, 4 (fallbacks packed per band position) and 8 GPUs (tested per token),
+    with 16 families whose offsets are odd and even."""
+    cfg = synth.CONFIGS["deepseek_v3"]
+    w = synth.make_workload("deepseek_v3", device="cuda", n_tokens=16 * 1500 + 37, layers=2, n_place=65)
+    ps = dict(w.placement_sets[0])
+    ps["home_start"] = ((np.arange(16) * band) % 32 // band * band).astype(np.int32)
+    ps["home_size"] = np.full(16, band, np.int32)
+    _score_both(w, ps, cfg.E)
+
+
 def test_eval_with_oracle_snapshot():
     cfg = synth.CONFIGS["deepseek_v3"]
     w = synth.make_workload("deepseek_v3", device="cuda", n_tokens=16 * 800, layers=2, n_place=70)
