@@ -6,8 +6,9 @@
 //   ev_zero      clear the workspace accumulators
 //   ev_flags     validate the placement tables; mark experts that have a secondary in any placement
 //   ev_replist   per layer: compact index of the marked ("replicated") experts
-//   ev_repinfo   per (placement, layer, replicated expert): feasible candidate mask FC and the
-//                fallback GPU argmin_{m in FC} load_ref (ties: lowest number)
+//   ev_repinfo   per (placement, layer, replicated expert): feasible candidate mask FC, the
+//                fallback GPU argmin_{m in FC} load_ref (ties: lowest number) and whether the expert
+//                has a single candidate in that placement
 //   ev_main      the trace pass (below); also counts every expert's dispatches and validates ids
 //   ev_finalize  loads = counts of single-candidate experts on their primary + replicated choices;
 //                costs from the accumulators
@@ -188,8 +189,11 @@ __global__ __launch_bounds__(256) void ev_repinfo(EvArgs a) {
     int best = -1;
     for (int m = 0; m < G; ++m)
       if (((fc >> m) & 1u) && (best < 0 || ref[m] < ref[best])) best = m;
+    // bit 31: the expert has a single candidate in this placement (it is served by its primary and
+    // belongs to the GPUs the token reaches before any multi-candidate slot is resolved)
+    const uint32_t single = (__popc(cand) == 1) ? 0x80000000u : 0u;
     a.ws.rep_info[(static_cast<int64_t>(l) * TACG_MAX_REPLICATED + r) * a.P + p] =
-        make_uint2(fc, static_cast<uint32_t>(best));
+        make_uint2(fc, static_cast<uint32_t>(best) | single);
   }
 }
 
@@ -459,12 +463,19 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
   uint8_t* rep_of = reinterpret_cast<uint8_t*>(ecnt + E);             // [E]
   const uint8_t* rep_of_g = a.ws.rep_of + static_cast<int64_t>(l) * E;
 
+  // one-hot primary GPU of every expert that has a single candidate in the placement; zero for the
+  // multi-candidate ones (they are resolved per token)
   for (int i = threadIdx.x; i < E * PW; i += blockDim.x) {
     const int e = i / PW, q = i - e * PW, p = p0 + q;
     uint32_t v = 0;
-    if (p < a.P && rep_of_g[e] == kNone) {
-      const uint8_t g = a.primary[(static_cast<int64_t>(p) * L + l) * E + e];
-      v = g < G ? (1u << g) : 0u;
+    if (p < a.P) {
+      const uint8_t r = rep_of_g[e];
+      const bool single = (r == kNone) ||
+          (a.ws.rep_info[(static_cast<int64_t>(l) * TACG_MAX_REPLICATED + r) * a.P + p].y >> 31);
+      if (single) {
+        const uint8_t g = a.primary[(static_cast<int64_t>(p) * L + l) * E + e];
+        v = g < G ? (1u << g) : 0u;
+      }
     }
     tbl[i] = v;
   }
@@ -477,6 +488,7 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
       const int r = i / PW, q = i - r * PW, p = p0 + q;
       uint2 v = make_uint2(1u, 0u);
       if (p < a.P) v = a.ws.rep_info[(static_cast<int64_t>(l) * TACG_MAX_REPLICATED + r) * a.P + p];
+      v.y &= 31u;
       uint32_t pack = 32u + v.y;  // bands wider than 4 GPUs: the plain fallback (+32)
       if (hz <= 4) {
         pack = 0;

@@ -248,6 +248,21 @@ def test_eval_band_widths(band):
     _score_both(w, ps, cfg.E)
 
 
+def test_eval_partial_replication():
+    """An expert with secondaries in some placements only: where it has a single candidate it is
+    served by its primary before the multi-candidate slots are resolved."""
+    cfg = synth.CONFIGS["deepseek_v3"]
+    w = synth.make_workload("deepseek_v3", device="cuda", n_tokens=16 * 1200 + 5, layers=2, n_place=70)
+    ps = dict(w.placement_sets[0])
+    sec = ps["secondary"].copy()
+    rng = np.random.default_rng(3)
+    drop = rng.random(sec.shape[:3]) < 0.5
+    sec[drop] = 0xFF
+    sec[:, :, :, 2][rng.random(sec.shape[:3]) < 0.3] = 0xFF       # some experts with fewer secondaries
+    ps["secondary"] = sec
+    _score_both(w, ps, cfg.E)
+
+
 def test_eval_with_oracle_snapshot():
     cfg = synth.CONFIGS["deepseek_v3"]
     w = synth.make_workload("deepseek_v3", device="cuda", n_tokens=16 * 800, layers=2, n_place=70)
