@@ -1,0 +1,117 @@
+"""GPU parity at the full workload sizes (the preset shapes at their full token, layer and placement
+counts, in the launch configuration the benchmark times).
+
+The oracle computes sampled outputs one by one (a few family/layer segments of the counts, the
+reweighted graph of sampled layers, a few scored placements over the whole trace); every other
+output is checked through properties that hold at any size (symmetry, diagonal, row sums and
+totals of the counts; per-layer load totals and cost bounds of the scores).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2606_01007_amd as tacg
+from paper_2606_01007_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    oracle.build()
+
+
+def _u32(t):
+    return tacg.as_u32(t)
+
+
+@pytest.mark.parametrize("name", ["deepseek16b", "qwen15", "qwen3_30b", "deepseek_v3"])
+def test_full_size(name):
+    cfg = synth.CONFIGS[name]
+    _say(f"[{name}] generating full workload")
+    w = synth.make_workload(name, device="cuda")
+    E, k, L, F = cfg.E, cfg.k, cfg.L, cfg.F
+    Ng = w.trace_group.shape[1]
+
+    # ---- co-activation counts: properties on every segment, oracle on sampled segments ----
+    D, C, err = tacg.coact_build(w.trace_group, w.fam_off_group, E)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    Dl, Cl = _u32(D), _u32(C)
+    nf = torch.as_tensor(np.diff(w.fam_off_group), device="cuda")
+    assert torch.equal(Cl, Cl.transpose(2, 3))
+    assert torch.equal(torch.diagonal(Cl, dim1=2, dim2=3), Dl)
+    assert torch.equal(Cl.sum(dim=3) - Dl, (k - 1) * Dl)
+    assert torch.equal(Dl.sum(dim=2), (nf[:, None] * k).expand(F, L))
+    tg = w.trace_group.cpu().numpy()
+    for f, l in [(0, 0), (F // 2, L // 2), (F - 1, L - 1)]:
+        Do, Co, e = oracle.coact_segment(tg, w.fam_off_group, E, f, l)
+        assert e == 0
+        np.testing.assert_array_equal(Dl[f, l].cpu().numpy(), Do)
+        np.testing.assert_array_equal(Cl[f, l].cpu().numpy(), Co)
+    _say(f"[{name}] counts ok")
+
+    # ---- reweighting: sampled layers against the oracle (counts recomputed by the oracle) ----
+    pref, at, _ = tacg.reweight(D, C, k)
+    for l in [0, L - 1]:
+        Dol = np.zeros((F, 1, E), np.int64)
+        Col = np.zeros((F, 1, E, E), np.int64)
+        for f in range(F):
+            Dol[f, 0], Col[f, 0], _ = oracle.coact_segment(tg, w.fam_off_group, E, f, l)
+        po, ato, _ = oracle.reweight(Dol, Col, k)
+        np.testing.assert_allclose(pref[l].cpu().double().numpy(), po[0], rtol=1e-5, atol=1e-30)
+        np.testing.assert_allclose(at[l].cpu().double().numpy(), ato[0], rtol=1e-5, atol=1e-30)
+    del tg
+    _say(f"[{name}] reweight ok")
+
+    # ---- placement scoring at full size: every placement set of the preset ----
+    ts = w.trace_serve.cpu().numpy()
+    Dso = None
+    for ps in w.placement_sets:
+        G, P = ps["n_gpus"], ps["primary"].shape[0]
+        prim = torch.as_tensor(ps["primary"]).cuda()
+        sec = torch.as_tensor(ps["secondary"]).cuda() if ps["secondary"] is not None else None
+        ref_g = ref_o = None
+        if sec is not None:
+            Ds, _, e1 = tacg.coact_build(w.trace_serve, w.fam_off_serve, E)
+            ref_g = tacg.placement_load(Ds, prim, G, err=e1)
+            if Dso is None:
+                Dso, _, _ = oracle.coact(ts, w.fam_off_serve, E)
+            ref_o = oracle.placement_load(Dso, ps["primary"], G)
+        out = tacg.eval_placements(w.trace_serve, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, prim,
+                                   sec, ref_g, theta=(3, 20))
+        jn, mv = tacg.jain_index(out["load"])
+        torch.cuda.synchronize()
+        assert int(out["err"].item()) == 0
+        if ref_g is not None:
+            np.testing.assert_array_equal(ref_g.cpu().numpy(), ref_o)
+        load = _u32(out["load"])
+        Ns = w.trace_serve.shape[1]
+        assert bool((load.sum(dim=2) == Ns * k).all())
+        ch, cs = out["cost_home"], out["cost_span"]
+        assert bool((ch >= 0).all()) and bool((ch <= Ns * L * min(k, G - 1)).all())
+        assert bool((cs >= 0).all()) and bool((cs <= Ns * L * (min(k, G) - 1)).all())
+        assert torch.equal(out["cost_home_fam"].sum(dim=1), ch)
+        for p in sorted({0, P // 2, P - 1}):
+            _say(f"[{name}] oracle scoring placement {p} of {P} (G={G})")
+            ro = oracle.score(ts, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, ps["primary"],
+                              ps["secondary"], ref_o, (3, 20), p_range=(p, p + 1))
+            assert ro["err"] == 0
+            assert int(ch[p]) == int(ro["cost_home"][p])
+            assert int(cs[p]) == int(ro["cost_span"][p])
+            np.testing.assert_array_equal(load[p].cpu().numpy(), ro["load"][p])
+            np.testing.assert_array_equal(out["cost_home_fam"][p].cpu().numpy(), ro["cost_home_fam"][p])
+            jo, vo = oracle.jain(ro["load"][p:p + 1])
+            np.testing.assert_allclose(float(jn[p]), jo[0], rtol=1e-5)
+            np.testing.assert_allclose(float(mv[p]), vo[0], rtol=1e-5, atol=1e-30)
+    _say(f"[{name}] scoring ok")
