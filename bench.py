@@ -68,11 +68,56 @@ def parse():
     ap.add_argument("--config", default="deepseek_v3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=0, help="layers of the oracle's scoring sample (0 = all)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/hbm_traffic.json from the counter_collection.csv files of two "
+                         "rocprofv3 --pmc runs of this script (FETCH_SIZE, then WRITE_SIZE) and exit")
     return ap.parse_args()
+
+
+# kernels whose HBM bytes are reported, and the device kernels each one is made of
+TRAFFIC_KERNELS = {"ev_main": ("ev_main",), "coact_build": ("coact_hist_kernel", "coact_reduce_kernel")}
+
+
+def write_traffic(fetch_csv: str, write_csv: str, workload: str) -> dict:
+    """Per-launch HBM bytes from rocprofv3 FETCH_SIZE / WRITE_SIZE counters (KiB per dispatch).
+
+    Each counter is scaled by what it reads for the 1 GiB device copy this script makes before the
+    timed region (the largest copy kernel of the run): bytes = KiB * 1024 * (2^30 / copy bytes)."""
+    import csv
+    import re
+    out = {"source_sha256": source_digest(), "kernels": {}, "scale": {}}
+    per = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        if not copies:
+            raise SystemExit(f"no copy kernel in {path}")
+        scale = CALIB_BYTES / (max(copies) * 1024.0)
+        out["scale"][counter] = scale
+        sums = {}
+        for r in rows:
+            m = re.search(r"tacg::\(anonymous namespace\)::(\w+)", r["Kernel_Name"])
+            if m:
+                sums.setdefault(m.group(1), []).append(float(r["Counter_Value"]) * 1024.0 * scale)
+        per[counter] = {k: sum(v) / len(v) for k, v in sums.items()}
+    for name, parts in TRAFFIC_KERNELS.items():
+        if all(p in per["FETCH_SIZE"] and p in per["WRITE_SIZE"] for p in parts):
+            f = sum(per["FETCH_SIZE"][p] for p in parts)
+            w = sum(per["WRITE_SIZE"][p] for p in parts)
+            out["kernels"][name] = {"workload": workload, "fetch_bytes": f, "write_bytes": w,
+                                    "bytes_per_launch": f + w}
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(out, fh, indent=1)
+        fh.write("\n")
+    return out
 
 
 def main():
     args = parse()
+    if args.traffic_from:
+        print(json.dumps(write_traffic(args.traffic_from[0], args.traffic_from[1], args.config)))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU; multi-GPU runs are not supported "
                                    "(the simulated GPU count G is a parameter of the workload, not of the launch)"}))

@@ -19,7 +19,7 @@ Paper passages followed (Sec. = section of the paper):
                        per-token dispatch sets; App. H "Comm"
   Jain, MaxVio         App. H eqs. jain, maxvio;  Comm. Red.: App. H eq. comm-red
 
-Readings where the paper is silent (also listed in the design doc):
+Readings where the paper is silent:
   * u = D / (N_f k) (sums to 1 over experts); A = C / N_f off the diagonal, A(e, e) = 0;
     N_f = sum_e D_f[l][e] / k (the family's token count).
   * z-score uses the population standard deviation; eps and tau are parameters.

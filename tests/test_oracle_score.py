@@ -3,7 +3,7 @@
 Scoring follows the per-token dispatch sets of App. C (cards_l = GPUs serving the token's experts at
 layer l; cross-group dispatch count max(0, |cards_l| - 1)) and the serving rule of Sec. 3.4 (eqs.
 mean-load, feasible-set and the fallback to the full candidate set).  The exact choice among
-feasible candidates is this build's reading (local first, then the anchor, then the least loaded),
+feasible candidates is a reading of that passage (local first, then the anchor, then the least loaded),
 so the GESR rule is pinned by hand-built cases and an independent brute force, not by the paper.
 """
 from fractions import Fraction
