@@ -30,6 +30,8 @@ namespace {
 
 constexpr int kMainThreads = 1024;
 constexpr int kMaxPieces = 160;
+constexpr uint32_t kXcds = 8;
+constexpr int64_t kTargetWorkgroups = 4096;  // XCDs of an MI355X; workgroups are dealt to them round-robin
 constexpr uint8_t kNone = 0xFF;
 
 struct EvWs {
@@ -73,6 +75,7 @@ struct EvArgs {
   int32_t L, K, E, F, G, P, R;
   int32_t theta_num, theta_den;
   int32_t n_pieces;
+  int32_t n_pblocks;  // placement blocks of 64 * PPL placements
   // One record per piece of one family's tokens: (first token, end token, family offset,
   // home_start | home_size << 8 | family << 16).  Kept as 16-byte records: indexing kernel-argument
   // arrays of different element sizes with one runtime index lets the compiler fold the byte and
@@ -202,8 +205,9 @@ __global__ __launch_bounds__(256) void ev_repinfo(EvArgs a) {
 // a workgroup scores 64 * PPL placements of one layer on one piece of one family's tokens.
 // grid (placement blocks, pieces, L).  The workgroups of placement block 0 also count the
 // dispatches of every expert and validate the ids (each token-layer is seen by exactly one of them).
-// Choices for replicated experts are counted in 16-bit LDS counters (two per dword), flushed to the
-// workspace after every round of at most 65535 / K tokens so that they cannot overflow.
+// Choices for replicated experts are counted in 16-bit LDS counters (two per dword).  After every
+// round of at most 65535 / K tokens (so that they cannot overflow) each thread adds a fixed set of
+// them into 32-bit registers and clears them; the registers go to the workspace once per workgroup.
 //
 // Per-token word `info` built by the lane that loaded the token-layer (wave-uniform after v_readlane):
 //   K <= 8:  bits 0-7 replicated-slot mask, 8-12 band position of the anchor GPU within its family's
@@ -335,6 +339,11 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
   constexpr int KB = S::KB;
   constexpr int U = 4;             // token-layers scored together (independent LDS reads in flight)
   constexpr uint32_t round_tokens = 65535u / K;
+  // each thread folds the same 2 * kRcntPerThread 16-bit counters after every round
+  constexpr int kRcntPerThread = (TACG_MAX_GPUS * PW / 2 + kMainThreads - 1) / kMainThreads;
+  uint32_t rsum[2 * kRcntPerThread];
+#pragma unroll
+  for (int c = 0; c < 2 * kRcntPerThread; ++c) rsum[c] = 0;
   const int E = a.E, G = a.G, L = a.L;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -424,19 +433,31 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
         sc.account(tinfo, m);
       }
     }
-    if (nrep > 0) {  // flush the 16-bit choice counters of this round (nrep is workgroup-uniform)
+    if (nrep > 0) {  // fold the 16-bit choice counters of this round into registers (nrep is workgroup-uniform)
       __syncthreads();
-      for (int i = threadIdx.x; i < G * PW / 2; i += blockDim.x) {
-        const uint32_t v = rcnt[i];
-        if (v) {
-          const int g = (2 * i) / PW, q = 2 * i - g * PW, p = p0 + q;
-          uint32_t* dst = a.ws.rep_load + (static_cast<int64_t>(p) * L + l) * G + g;
-          if (p < a.P && (v & 0xffffu)) atomicAdd(dst, v & 0xffffu);
-          if (p + 1 < a.P && (v >> 16)) atomicAdd(dst + static_cast<int64_t>(L) * G, v >> 16);
+#pragma unroll
+      for (int c = 0; c < kRcntPerThread; ++c) {
+        const int i = threadIdx.x + c * kMainThreads;
+        if (i < G * PW / 2) {
+          const uint32_t v = rcnt[i];
+          rsum[2 * c] += v & 0xffffu;
+          rsum[2 * c + 1] += v >> 16;
           rcnt[i] = 0;
         }
       }
       __syncthreads();
+    }
+  }
+  if (nrep > 0) {  // one global add per counter and workgroup
+#pragma unroll
+    for (int c = 0; c < kRcntPerThread; ++c) {
+      const int i = threadIdx.x + c * kMainThreads;
+      if (i < G * PW / 2) {
+        const int g = (2 * i) / PW, q = 2 * i - g * PW, p = p0 + q;
+        uint32_t* dst = a.ws.rep_load + (static_cast<int64_t>(p) * L + l) * G + g;
+        if (p < a.P && rsum[2 * c]) atomicAdd(dst, rsum[2 * c]);
+        if (p + 1 < a.P && rsum[2 * c + 1]) atomicAdd(dst + static_cast<int64_t>(L) * G, rsum[2 * c + 1]);
+      }
     }
   }
 
@@ -452,7 +473,16 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
   extern __shared__ __align__(16) uint32_t lds[];
   constexpr int PW = 64 * PPL;
   const int E = a.E, G = a.G, L = a.L;
-  const int pb = blockIdx.x, piece = blockIdx.y, l = blockIdx.z;
+  // XCD-aware order: the hardware hands workgroup b to XCD b mod 8, so each XCD takes a contiguous
+  // run of virtual ids v, in which the placement blocks of one (piece, layer) tile are adjacent.
+  // They run together on that XCD and share its L2 for the tile's trace rows.
+  const uint32_t total = gridDim.x, b = blockIdx.x;
+  const uint32_t xcd = b % kXcds, per = total / kXcds, rem = total % kXcds;
+  const uint32_t v = xcd * per + min(xcd, rem) + b / kXcds;
+  const int npb = a.n_pblocks;
+  const int pb = static_cast<int>(v % npb);
+  const int tile = static_cast<int>(v / npb);
+  const int piece = tile % a.n_pieces, l = tile / a.n_pieces;
   const int p0 = pb * PW;
   const int nrep = a.ws.n_rep[l];
   const bool counter = (pb == 0);
@@ -577,7 +607,11 @@ int launch_main(const EvArgs& a, int n_pblocks, hipStream_t stream) {
                      static_cast<size_t>(a.G) * PW * 2 + static_cast<size_t>(a.E) * 4 + align256(a.E);
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&ev_main<K, PPL>), hipFuncAttributeMaxDynamicSharedMemorySize,
                       static_cast<int>(lds));
-  hipLaunchKernelGGL((ev_main<K, PPL>), dim3(n_pblocks, a.n_pieces, a.L), dim3(kMainThreads), lds, stream, a);
+  EvArgs b = a;
+  b.n_pblocks = n_pblocks;
+  const int64_t grid = static_cast<int64_t>(n_pblocks) * a.n_pieces * a.L;
+  if (grid > 0x7fffffff) return TACG_E_UNSUPPORTED;
+  hipLaunchKernelGGL((ev_main<K, PPL>), dim3(static_cast<uint32_t>(grid)), dim3(kMainThreads), lds, stream, b);
   return TACG_OK;
 }
 
@@ -678,9 +712,12 @@ int launch_eval(const int16_t* trace, int64_t N, int32_t L, int32_t K, int32_t E
   a.R = R;
   a.theta_num = theta_num;
   a.theta_den = theta_den;
-  // pieces: split every family's tokens into chunks of about N / 64 tokens (at least 4096, at
-  // most 2^26 so that the per-lane 32-bit cost accumulators cannot overflow)
-  int64_t chunk = std::min<int64_t>(int64_t(1) << 26, std::max<int64_t>(4096, (N + 63) / 64));
+  // pieces: split every family's tokens into chunks sized for about kTargetWorkgroups workgroups of
+  // ev_main (at least 4096 tokens; at most 2^26 so that the per-lane 32-bit cost accumulators cannot
+  // overflow).  Fewer, longer workgroups amortise the table set-up and the per-workgroup flushes.
+  const int64_t n_pblocks = E > 64 ? (P + 127) / 128 : (P + 255) / 256;
+  int64_t chunk = (N * n_pblocks * L + kTargetWorkgroups - 1) / kTargetWorkgroups;
+  chunk = std::min<int64_t>(int64_t(1) << 26, std::max<int64_t>(4096, chunk));
   int np = 0;
   for (;;) {
     np = 0;
