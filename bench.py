@@ -67,6 +67,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", default="deepseek_v3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-quality", action="store_true", help="skip the untimed placement-quality context")
     ap.add_argument("--cpu-layers", type=int, default=0, help="layers of the oracle's scoring sample (0 = all)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/hbm_traffic.json from the counter_collection.csv files of two "
@@ -260,9 +261,59 @@ def main():
     }
 
     log(f"timed {args.steps} steps: {wall / args.steps * 1e3:.1f} ms/step")
+    if not args.no_quality:
+        result["placement_quality"] = placement_quality(w, ps, cfg, D, C, err)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, ps, cfg, args.cpu_layers)
     print(json.dumps(result), flush=True)
+
+
+def placement_quality(w, ps, cfg, D, C, err):
+    """Untimed context: the paper's communication metric (App. H "Comm": mean over tokens of
+    sum_l (|cards_l| - 1)) on the serving trace, for the contiguous default placement and for the
+    TACG placement grouped on the host from this run's A-tilde (grouping trace) with GESR replicas
+    (generic experts by centrality, secondaries by affinity), plus Jain and MaxVio."""
+    import numpy as np
+    import torch
+
+    import paper_2606_01007_amd as tacg
+    from paper_2606_01007_amd import placement as pm
+
+    t0 = time.time()
+    E, k, L = cfg.E, cfg.k, cfg.L
+    G, cap = ps["n_gpus"], ps["capacity"]
+    n_rep, n_sec = cfg.placements[0].n_generic_rep, cfg.placements[0].n_secondary
+    _, at, ah = tacg.reweight(D, C, k, alpha=0.25, tau=1.0, eps=1e-8, want_hat=True)
+    at, ah = at.cpu().double().numpy(), ah.cpu().double().numpy()
+    default = np.repeat(np.arange(G, dtype=np.uint8), pm.capacities(E, G, cap))[None].repeat(L, axis=0)
+    grouped = pm.tacg_placement(at, G, cap)
+    prim = np.stack([default, grouped])                                    # [2][L][E]
+    sec = None
+    if n_sec > 0:
+        gen = pm.generic_experts(ah, n_rep)
+        sec = np.stack([pm.affinity_secondaries(ah, prim[i], gen, G, n_sec) for i in range(2)])
+    dev = "cuda"
+    prim_t = torch.as_tensor(prim).to(dev)
+    sec_t = torch.as_tensor(sec).to(dev) if sec is not None else None
+    ref = None
+    if sec_t is not None:
+        Ds, _, _ = tacg.coact_build(w.trace_serve, w.fam_off_serve, E, err=err)
+        ref = tacg.placement_load(Ds, prim_t, G, err=err)
+    out = tacg.eval_placements(w.trace_serve, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, prim_t,
+                               sec_t, ref, theta=(3, 20), err=err)
+    jn, mv = tacg.jain_index(out["load"])
+    torch.cuda.synchronize()
+    Ns = w.trace_serve.shape[1]
+    span = out["cost_span"].cpu().numpy().astype(np.float64) / Ns
+    home = out["cost_home"].cpu().numpy().astype(np.float64) / Ns
+    return {"placements": "contiguous default vs TACG (host spectral grouping of this run's A-tilde, alpha=0.25)"
+                          f" with GESR ({n_rep} generic experts by centrality x {n_sec} secondaries by affinity)",
+            "trace": "serving trace (synthetic)",
+            "comm_default": span[0], "comm_tacg": span[1],
+            "comm_reduction_pct": 100.0 * (span[0] - span[1]) / span[0] if span[0] > 0 else None,
+            "home_cost_default": home[0], "home_cost_tacg": home[1],
+            "jain": [float(jn[0]), float(jn[1])], "maxvio": [float(mv[0]), float(mv[1])],
+            "host_s": time.time() - t0}
 
 
 def cpu_baseline(w, ps, cfg, cpu_layers):

@@ -22,6 +22,9 @@
 namespace tacg {
 namespace {
 
+constexpr int kReduceThreads = 1024;
+constexpr int kDepth = 4;  // token-layers per thread in flight in coact_hist_kernel
+
 struct CoactArgs {
   const int16_t* trace;
   int64_t N;           // tokens
@@ -64,46 +67,103 @@ constexpr int next_pow2(int k) { return k <= 1 ? 1 : 2 * next_pow2((k + 1) / 2);
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// The k ids of one token-layer as unsigned 16-bit values (negative ids become >= 32768 >= E).
+// The raw k ids of one token-layer, fetched with the widest aligned loads (rows of k int16 are
+// 2k bytes, so even k allows 4-, 8- or 16-byte loads), and unpacked to unsigned 16-bit values
+// (negative ids become >= 32768 >= E).  Fetch and unpack are separate so that the next token-layer's
+// loads are in flight while the current one is counted.
 template <int K>
-__device__ __forceinline__ void load_ids(const int16_t* __restrict__ p, uint32_t* x) {
-  if constexpr (K % 8 == 0) {
+struct RawIds {
+  static constexpr int kWords = (K % 2 == 0) ? K / 2 : K;  // dwords (even k) or halfwords (odd k)
+  uint32_t w[kWords];
+
+  __device__ __forceinline__ void fetch(const int16_t* __restrict__ p) {
+    if constexpr (K % 8 == 0) {
 #pragma unroll
-    for (int q = 0; q < K / 8; ++q) {
-      const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p) + q);
-      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+      for (int q = 0; q < K / 8; ++q) {
+        const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p) + q);
+        w[4 * q] = v.x;
+        w[4 * q + 1] = v.y;
+        w[4 * q + 2] = v.z;
+        w[4 * q + 3] = v.w;
+      }
+    } else if constexpr (K % 4 == 0) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        x[8 * q + 2 * r] = w[r] & 0xffffu;
-        x[8 * q + 2 * r + 1] = w[r] >> 16;
+      for (int q = 0; q < K / 4; ++q) {
+        const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p) + q);
+        w[2 * q] = v.x;
+        w[2 * q + 1] = v.y;
+      }
+    } else if constexpr (K % 2 == 0) {
+#pragma unroll
+      for (int q = 0; q < K / 2; ++q) w[q] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p) + q);
+    } else {
+#pragma unroll
+      for (int q = 0; q < K; ++q) w[q] = static_cast<uint16_t>(p[q]);
+    }
+  }
+
+  __device__ __forceinline__ void unpack(uint32_t* x) const {
+    if constexpr (K % 2 == 0) {
+#pragma unroll
+      for (int q = 0; q < K / 2; ++q) {
+        x[2 * q] = w[q] & 0xffffu;
+        x[2 * q + 1] = w[q] >> 16;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < K; ++q) x[q] = w[q];
+    }
+  }
+};
+
+// Count one token-layer into the workgroup's triangle (see the file comment).
+template <int K>
+__device__ __forceinline__ void count_token(const RawIds<K>& raw, bool valid, uint32_t* hist, uint32_t E,
+                                            uint32_t& err) {
+  constexpr int NP2 = next_pow2(K);
+  uint32_t v[NP2];
+  raw.unpack(v);
+#pragma unroll
+  for (int i = K; i < NP2; ++i) v[i] = 0xffffu;
+  if constexpr (K == 1) {
+    if (valid) {
+      if (v[0] < E) {
+        __hip_atomic_fetch_add(&hist[v[0]], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      } else {
+        err |= TACG_ERR_ID_RANGE;
       }
     }
-  } else if constexpr (K % 4 == 0) {
-#pragma unroll
-    for (int q = 0; q < K / 4; ++q) {
-      const u32x2 v = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p) + q);
-      x[4 * q] = v.x & 0xffffu;
-      x[4 * q + 1] = v.x >> 16;
-      x[4 * q + 2] = v.y & 0xffffu;
-      x[4 * q + 3] = v.y >> 16;
-    }
-  } else if constexpr (K % 2 == 0) {
-#pragma unroll
-    for (int q = 0; q < K / 2; ++q) {
-      const uint32_t v = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p) + q);
-      x[2 * q] = v & 0xffffu;
-      x[2 * q + 1] = v >> 16;
-    }
   } else {
+    sort_network<NP2>(v);
+    bool dup = false;
 #pragma unroll
-    for (int q = 0; q < K; ++q) x[q] = static_cast<uint16_t>(p[q]);
+    for (int i = 0; i + 1 < K; ++i) dup |= (v[i] == v[i + 1]);
+    const bool range_bad = v[K - 1] >= E;
+    if (valid && (dup | range_bad)) {
+      err |= (range_bad ? TACG_ERR_ID_RANGE : 0u) | (dup ? TACG_ERR_ID_DUP : 0u);
+    } else if (valid) {
+      // byte offset of the triangle row of each id taken as the smaller member of a pair:
+      // 4 * (x (2E - 3 - x) / 2 - 1) = x (2 (2E - 3) - 2x) - 4; both factors fit 24 bits
+      const uint32_t rbk = 2u * (2u * E - 3u);
+      uint32_t rb[K - 1];
+#pragma unroll
+      for (int i = 0; i < K - 1; ++i) rb[i] = __umul24(v[i], rbk - 2u * v[i]) - 4u;
+#pragma unroll
+      for (int i = 0; i < K - 1; ++i) {
+#pragma unroll
+        for (int j = i + 1; j < K; ++j) {
+          uint32_t* cell = reinterpret_cast<uint32_t*>(
+              __builtin_assume_aligned(reinterpret_cast<char*>(hist) + (rb[i] + 4u * v[j]), 4));
+          __hip_atomic_fetch_add(cell, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+      }
+    }
   }
 }
 
 template <int K>
 __global__ __launch_bounds__(kCoactThreads) void coact_hist_kernel(CoactArgs a) {
   extern __shared__ uint32_t hist[];
-  constexpr int NP2 = next_pow2(K);
   const int tid = threadIdx.x;
   const int nb = a.nbins;
   for (int i = tid; i < nb; i += blockDim.x) hist[i] = 0u;
@@ -113,7 +173,6 @@ __global__ __launch_bounds__(kCoactThreads) void coact_hist_kernel(CoactArgs a) 
   int64_t pos = (w * a.total) / a.W;
   const int64_t end = ((w + 1) * a.total) / a.W;
   const uint32_t E = static_cast<uint32_t>(a.E);
-  const uint32_t rbk = 2u * (2u * E - 3u);
   uint32_t err = 0;
 
   while (pos < end) {
@@ -122,40 +181,24 @@ __global__ __launch_bounds__(kCoactThreads) void coact_hist_kernel(CoactArgs a) 
     int f = 0;
     while (a.fam_off[f + 1] <= t) ++f;
     const int64_t stop = min(end, l * a.N + a.fam_off[f + 1]);
-    for (int64_t x = pos + tid; x < stop; x += blockDim.x) {
-      uint32_t v[NP2];
-      load_ids<K>(a.trace + x * K, v);
+    // one token-layer per thread and step.  The ids of the next kDepth - 1 steps are in flight in
+    // a ring of buffers while one step is counted; fetch addresses are clamped to the segment's last
+    // token-layer, so every load is unconditional and in bounds, and the loop is workgroup-uniform
+    // (a thread past the end of the segment fetches and sorts but does not count).
+    const int64_t bd = blockDim.x, last = stop - 1;
+    RawIds<K> ring[kDepth];
 #pragma unroll
-      for (int i = K; i < NP2; ++i) v[i] = 0xffffu;
-      if constexpr (K == 1) {
-        if (v[0] < E) {
-          __hip_atomic_fetch_add(&hist[v[0]], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        } else {
-          err |= TACG_ERR_ID_RANGE;
-        }
-      } else {
-        sort_network<NP2>(v);
-        bool dup = false;
+    for (int d = 0; d < kDepth; ++d) {
+      ring[d].fetch(a.trace + min(pos + tid + d * bd, last) * K);
+      // keep the issue order ring[0], ring[1], ...: the loop below then waits for one buffer at a time
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int64_t xb = pos; xb < stop; xb += kDepth * bd) {
 #pragma unroll
-        for (int i = 0; i + 1 < K; ++i) dup |= (v[i] == v[i + 1]);
-        const bool range_bad = v[K - 1] >= E;
-        if (dup | range_bad) {
-          err |= (range_bad ? TACG_ERR_ID_RANGE : 0u) | (dup ? TACG_ERR_ID_DUP : 0u);
-        } else {
-          // byte offset of the triangle row of each id taken as the smaller member of a pair
-          uint32_t rb[K - 1];
-#pragma unroll
-          for (int i = 0; i < K - 1; ++i) rb[i] = v[i] * (rbk - 2u * v[i]) - 4u;
-#pragma unroll
-          for (int i = 0; i < K - 1; ++i) {
-#pragma unroll
-            for (int j = i + 1; j < K; ++j) {
-              uint32_t* cell = reinterpret_cast<uint32_t*>(__builtin_assume_aligned(
-                  reinterpret_cast<char*>(hist) + (rb[i] + 4u * v[j]), 4));
-              __hip_atomic_fetch_add(cell, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-            }
-          }
-        }
+      for (int d = 0; d < kDepth; ++d) {
+        const int64_t x = xb + d * bd + tid;
+        count_token<K>(ring[d], x < stop, hist, E, err);
+        ring[d].fetch(a.trace + min(x + kDepth * bd, last) * K);
       }
     }
     __syncthreads();
@@ -175,9 +218,12 @@ __device__ __forceinline__ int64_t owner_of(int64_t x, int64_t total, int64_t W)
   return ((x + 1) * W + total - 1) / total - 1;
 }
 
-// One workgroup per segment s = l * F + f.  Each wave takes rows i; lanes take columns j.
-__global__ __launch_bounds__(256) void coact_reduce_kernel(CoactArgs a, uint32_t* __restrict__ D,
-                                                           uint32_t* __restrict__ C, uint32_t accumulate) {
+// One workgroup per segment s = l * F + f.  The partial triangles of the workgroups that touched
+// the segment are summed into LDS with coalesced reads; then each wave writes dense rows i of C
+// (lanes over columns j, coalesced) from the LDS triangle and recovers D_i from the row sum.
+__global__ __launch_bounds__(kReduceThreads) void coact_reduce_kernel(CoactArgs a, uint32_t* __restrict__ D,
+                                                                      uint32_t* __restrict__ C, uint32_t accumulate) {
+  extern __shared__ uint32_t tri[];
   const int s = blockIdx.x;
   const int l = s / a.F, f = s % a.F;
   const int E = a.E;
@@ -188,42 +234,40 @@ __global__ __launch_bounds__(256) void coact_reduce_kernel(CoactArgs a, uint32_t
     w0 = owner_of(seg0, a.total, a.W);
     w1 = owner_of(seg1 - 1, a.total, a.W);
   }
+  const int nb = a.nbins;
+  for (int b = threadIdx.x; b < nb; b += blockDim.x) {
+    uint32_t v = 0;
+    for (int64_t w = w0; w <= w1; ++w) v += __builtin_nontemporal_load(&a.partial[(w + s) * static_cast<int64_t>(nb) + b]);
+    tri[b] = v;
+  }
+  __syncthreads();
+
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int nwaves = blockDim.x >> 6;
   uint32_t* Dseg = D + (static_cast<int64_t>(f) * a.L + l) * E;
   uint32_t* Cseg = C + (static_cast<int64_t>(f) * a.L + l) * E * static_cast<int64_t>(E);
-  const int64_t nb = a.nbins;
-
   for (int i = wave; i < E; i += nwaves) {
     uint32_t rowsum = 0;
+    uint32_t* crow = Cseg + static_cast<int64_t>(i) * E;
     for (int j = lane; j < E; j += 64) {
+      if (j == i) continue;  // the diagonal is written below, from the row sum
       uint32_t v = 0;
-      if (a.K == 1) {
-        if (j == i)
-          for (int64_t w = w0; w <= w1; ++w) v += a.partial[(w + s) * nb + i];
-      } else if (j != i) {
+      if (a.K > 1) {
         const uint32_t lo = min(i, j), hi = max(i, j);
-        const uint32_t T = lo * (2u * E - 3u - lo) / 2u - 1u + hi;
-        for (int64_t w = w0; w <= w1; ++w) v += a.partial[(w + s) * nb + T];
+        v = tri[lo * (2u * E - 3u - lo) / 2u - 1u + hi];
         rowsum += v;
       }
-      if (j != i) {
-        uint32_t* c = Cseg + static_cast<int64_t>(i) * E + j;
-        *c = accumulate ? *c + v : v;
-      } else if (a.K == 1) {
-        rowsum = v;
-      }
+      crow[j] = accumulate ? crow[j] + v : v;
     }
-    // wave reduction of the row sum -> D_i
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) rowsum += __shfl_xor(rowsum, o, 64);
     if (lane == 0) {
-      const uint32_t d = (a.K == 1) ? rowsum : rowsum / static_cast<uint32_t>(a.K - 1);
-      uint32_t* c = Cseg + static_cast<int64_t>(i) * E + i;
+      // each valid token with expert i adds k - 1 pairs to row i; with k = 1 the bins are D itself
+      const uint32_t d = (a.K == 1) ? tri[i] : rowsum / static_cast<uint32_t>(a.K - 1);
       const uint32_t dn = accumulate ? Dseg[i] + d : d;
       Dseg[i] = dn;
-      *c = dn;
+      crow[i] = dn;
     }
   }
 }
@@ -281,7 +325,9 @@ int launch_coact(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32
     if (hipGetLastError() != hipSuccess) return TACG_E_DEVICE;
   }
   if (a.total == 0) a.total = 1;  // the reduction sees no contributors (all segments empty)
-  hipLaunchKernelGGL(coact_reduce_kernel, dim3(n_layers * n_fam), dim3(256), 0, stream, a, D, C,
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&coact_reduce_kernel),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  hipLaunchKernelGGL(coact_reduce_kernel, dim3(n_layers * n_fam), dim3(kReduceThreads), lds, stream, a, D, C,
                      (flags & TACG_ACCUMULATE) ? 1u : 0u);
   if (hipGetLastError() != hipSuccess) return TACG_E_DEVICE;
   return TACG_OK;

@@ -312,3 +312,41 @@ def test_jain_parity():
     jo, vo = oracle.jain(ld, per_layer=True)
     _close(j, jo)
     _close(v, vo)
+
+
+# ------------------------------------------------------------------------------------------------
+# host placement inputs (TACG grouping, GESR tables) built from the oracle's graph, scored by both
+# ------------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("name,setidx", [("qwen15", 0), ("qwen3_30b", 0)])
+def test_tacg_placement_scored(name, setidx):
+    from paper_2606_01007_amd import placement as pm
+    _say(f"tacg placement {name} set {setidx}")
+    cfg = synth.CONFIGS[name]
+    w = synth.make_workload(name, device="cuda", n_tokens=24000, n_place=2, layers=3)
+    ps = w.placement_sets[setidx]
+    G, cap = ps["n_gpus"], ps["capacity"]
+    spec = cfg.placements[setidx]
+    tg = w.trace_group.cpu().numpy()
+    Do, Co, _ = oracle.coact(tg, w.fam_off_group, cfg.E)
+    _, at_o, ah_o = oracle.reweight(Do, Co, cfg.k, alpha=0.25)
+    L = tg.shape[0]
+    default = np.repeat(np.arange(G, dtype=np.uint8), pm.capacities(cfg.E, G, cap))[None].repeat(L, axis=0)
+    prim = np.stack([default, pm.tacg_placement(at_o, G, cap)])
+    gen = pm.generic_experts(ah_o, spec.n_generic_rep)
+    sec = np.stack([pm.affinity_secondaries(ah_o, prim[i], gen, G, spec.n_secondary) for i in range(2)])
+    ts = w.trace_serve.cpu().numpy()
+    Dso, _, _ = oracle.coact(ts, w.fam_off_serve, cfg.E)
+    ref_o = oracle.placement_load(Dso, prim, G)
+    ro = oracle.score(ts, w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], G, prim, sec, ref_o, (3, 20))
+    prim_t, sec_t = torch.as_tensor(prim).cuda(), torch.as_tensor(sec).cuda()
+    Ds, _, e1 = tacg.coact_build(w.trace_serve, w.fam_off_serve, cfg.E)
+    ref_g = tacg.placement_load(Ds, prim_t, G, err=e1)
+    out = tacg.eval_placements(w.trace_serve, w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], G, prim_t,
+                               sec_t, ref_g, theta=(3, 20))
+    assert _err(out["err"]) == 0 and _err(e1) == 0
+    np.testing.assert_array_equal(ref_g.cpu().numpy(), ref_o)
+    np.testing.assert_array_equal(out["cost_span"].cpu().numpy(), ro["cost_span"])
+    np.testing.assert_array_equal(out["cost_home"].cpu().numpy(), ro["cost_home"])
+    np.testing.assert_array_equal(_u32(out["load"]), ro["load"])
+    # the grouped placement co-locates the planted clusters: fewer GPUs spanned than the default
+    assert ro["cost_span"][1] < ro["cost_span"][0]
