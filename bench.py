@@ -68,6 +68,8 @@ def parse():
     ap.add_argument("--config", default="deepseek_v3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-quality", action="store_true", help="skip the untimed placement-quality context")
+    ap.add_argument("--tokens", type=int, default=0, help="tokens per trace (0 = the preset's; for profiling runs)")
+    ap.add_argument("--layers", type=int, default=0, help="MoE layers (0 = the preset's; for profiling runs)")
     ap.add_argument("--cpu-layers", type=int, default=0, help="layers of the oracle's scoring sample (0 = all)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/hbm_traffic.json from the counter_collection.csv files of two "
@@ -135,12 +137,13 @@ def main():
     dev = "cuda"
     cfg = synth.CONFIGS[args.config]
     t0 = time.time()
-    w = synth.make_workload(args.config, device=dev)
+    w = synth.make_workload(args.config, device=dev, n_tokens=args.tokens or None, layers=args.layers or None)
     torch.cuda.synchronize()
     gen_s = time.time() - t0
     log(f"generated {args.config} in {gen_s:.1f} s")
     ps = w.placement_sets[0]
-    E, k, L, F = cfg.E, cfg.k, cfg.L, cfg.F
+    E, k, F = cfg.E, cfg.k, cfg.F
+    L = w.trace_group.shape[0]
     G, P = ps["n_gpus"], ps["primary"].shape[0]
     Ng, Ns = w.trace_group.shape[1], w.trace_serve.shape[1]
     prim = torch.as_tensor(ps["primary"]).to(dev)
@@ -173,6 +176,7 @@ def main():
     del calib_src, calib_dst
 
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    reduced = bool(args.tokens or args.layers)
 
     def step(timed):
         if timed:
@@ -232,7 +236,8 @@ def main():
         "dtype": "u32",
         "data": "synthetic",
         "config": {
-            "workload": f"{cfg.name}: E={E} top-{k} L={L} F={F}, grouping trace {Ng} tokens (uniform mix), "
+            "workload": f"{cfg.name}{' (reduced for profiling)' if args.tokens or args.layers else ''}: "
+                        f"E={E} top-{k} L={L} F={F}, grouping trace {Ng} tokens (uniform mix), "
                         f"serving trace {Ns} tokens ({cfg.serve_mix} mix), {P} placements on G={G} cap "
                         f"{ps['capacity']}, replicas {cfg.placements[0].n_generic_rep}x{cfg.placements[0].n_secondary}"
                         f", theta=3/20",
@@ -249,13 +254,13 @@ def main():
         "roofline": {"kernel": "ev_main (tacg_eval_placements)", "bound": "alu",
                      "achieved": eval_tops, "peak": VALU_PEAK_TOPS, "unit": "TFLOP/s",
                      "frac": eval_tops / VALU_PEAK_TOPS,
-                     "traffic": measured_traffic("ev_main", cfg.name),
+                     "traffic": None if reduced else measured_traffic("ev_main", cfg.name),
                      "note": "int32 lane-ops per placement-token-layer: k-1 ORs of one-hot GPU masks, "
                              "one and-not and two popcounts; peak = 256 CUs x 64 lanes x 2.4 GHz"},
         "roofline_coact": {"kernel": "coact_hist + coact_reduce (tacg_coact_build)", "bound": "hbm",
                            "achieved": coact_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": coact_gbs / HBM_PEAK_GBS,
-                           "traffic": measured_traffic("coact_build", cfg.name),
+                           "traffic": None if reduced else measured_traffic("coact_build", cfg.name),
                            "note": "algorithmic bytes: the int16 trace once + dense C and D written"},
         "gen_s": gen_s,
     }
@@ -280,7 +285,8 @@ def placement_quality(w, ps, cfg, D, C, err):
     from paper_2606_01007_amd import placement as pm
 
     t0 = time.time()
-    E, k, L = cfg.E, cfg.k, cfg.L
+    E, k = cfg.E, cfg.k
+    L = w.trace_group.shape[0]
     G, cap = ps["n_gpus"], ps["capacity"]
     n_rep, n_sec = cfg.placements[0].n_generic_rep, cfg.placements[0].n_secondary
     _, at, ah = tacg.reweight(D, C, k, alpha=0.25, tau=1.0, eps=1e-8, want_hat=True)
@@ -351,7 +357,7 @@ def cpu_baseline(w, ps, cfg, cpu_layers):
             "sample": f"co-activation build of the whole grouping trace ({w.trace_group.shape[1]} tokens x "
                       f"{w.trace_group.shape[0]} layers, {t_coact:.1f} s); scoring of placement 0 on the serving "
                       f"trace over {Ls} layers ({t_score:.1f} s)",
-            "scoring_value": Ns * Ls / cfg.L / t_score if Ls else None,
+            "scoring_value": Ns * Ls / w.trace_serve.shape[0] / t_score if Ls else None,
             "scoring_unit": "placements×tokens/s (one placement over all layers, scaled from the sample)",
             "err": int(e1) | int(r["err"])}
 

@@ -51,7 +51,8 @@ def build(force: bool = False) -> str:
     """Compile tacg_oracle.c with gcc into liboracle.so (next to the source)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-o", tmp, _SRC], check=True)
+        subprocess.run(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-ffp-contract=off", "-o", tmp, _SRC,
+                        "-lm"], check=True)
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -71,6 +72,9 @@ def _load():
             lib.oracle_score.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, i32, i32,
                                          P, P, i32, P, i32, i32, P, P, P, P]
             lib.oracle_score.restype = ctypes.c_int
+            lib.oracle_score_online.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, i32, i32,
+                                                P, P, i32, ctypes.c_double, i32, i32, P, P, P, P, P, P]
+            lib.oracle_score_online.restype = ctypes.c_int
             lib.oracle_num_threads.restype = ctypes.c_int
             _lib = lib
     return _lib
@@ -226,6 +230,39 @@ def score(trace, fam_off, n_experts: int, home_start, home_size, n_gpus: int, pr
                                _ptr(prim), _ptr(sec), R, _ptr(ref), int(tn), int(td),
                                _ptr(cost_home), _ptr(cost_span), _ptr(load), _ptr(fam))
     return dict(cost_home=cost_home, cost_span=cost_span, load=load, cost_home_fam=fam, err=int(err))
+
+
+def score_online(trace, fam_off, n_experts: int, home_start, home_size, n_gpus: int, primary,
+                 secondary=None, rho: float = 0.995, theta=(3, 20), state=None, p_range=None):
+    """Sequential serving with decayed per-GPU loads (Sec. 3.4, eq. load-update); see
+    oracle_score_online in tacg_oracle.c.  state: float64 [P][L][G] initial loads (None = zero).
+    Returns dict(cost_home, cost_span, load, cost_home_fam, state (final loads), err)."""
+    tr = _np(trace, np.int16)
+    L, N, k = tr.shape
+    off = _np(fam_off, np.int64)
+    F = off.size - 1
+    hs = _np(home_start, np.int32)
+    hz = _np(home_size, np.int32)
+    prim = _np(primary, np.uint8)
+    P = prim.shape[0]
+    if secondary is not None and secondary.shape[-1] > 0:
+        sec = _np(secondary, np.uint8)
+        R = sec.shape[-1]
+    else:
+        sec, R = None, 0
+    p0, p1 = p_range if p_range is not None else (0, P)
+    st_in = None if state is None else _np(state, np.float64)
+    st_out = np.zeros((P, L, n_gpus), dtype=np.float64)
+    cost_home = np.zeros(P, dtype=np.int64)
+    cost_span = np.zeros(P, dtype=np.int64)
+    load = np.zeros((P, L, n_gpus), dtype=np.int64)
+    fam = np.zeros((P, F), dtype=np.int64)
+    tn, td = theta if theta is not None else (0, 0)
+    err = _load().oracle_score_online(_ptr(tr), N, L, k, n_experts, _ptr(off), F, _ptr(hs), _ptr(hz), n_gpus, P,
+                                      p0, p1, _ptr(prim), _ptr(sec), R, float(rho), int(tn), int(td), _ptr(st_in),
+                                      _ptr(st_out), _ptr(cost_home), _ptr(cost_span), _ptr(load), _ptr(fam))
+    return dict(cost_home=cost_home, cost_span=cost_span, load=load, cost_home_fam=fam, state=st_out,
+                err=int(err))
 
 
 # ------------------------------------------------------------------------------------------------

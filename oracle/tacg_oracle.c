@@ -28,6 +28,7 @@
  *     candidate of smallest load, ties to the lowest GPU number; add the choice to R;
  *   - the anchor (home) GPU of the t-th token of family f is home_start[f] + (t mod home_size[f]).
  */
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -227,6 +228,145 @@ int oracle_score(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32
                 for (int32_t s = 0; s < k; ++s) ld[slot_gpu[s]] += 1;
             }
         }
+#pragma omp atomic
+        cost_home[p] += home_acc;
+#pragma omp atomic
+        cost_span[p] += span_acc;
+        if (cost_home_fam)
+            for (int32_t f = 0; f < n_fam && f < 64; ++f) {
+#pragma omp atomic
+                cost_home_fam[(int64_t)p * n_fam + f] += fam_acc[f];
+            }
+    }
+    return err;
+}
+
+/*
+ * Serving with decayed loads (Sec. 3.4 in its sequential form, eqs. mean-load, feasible-set and
+ * load-update): the same per-token choice as oracle_score, but the loads L_m that the guard and the
+ * least-loaded fallback read are exponentially decayed per-GPU dispatch loads, updated after every
+ * token in trace order:
+ *     L_m <- rho * L_m + Delta_m       (Delta_m = the token's slots served by m; one fused
+ *                                       multiply-add in float64)
+ * Each (placement, layer) keeps its own loads, starting from state[p][l][.] (zero when state is NULL)
+ * and leaving the final loads there when state_out is not NULL.  The guard is the rational form
+ * theta_den * G * L_m <= (theta_den + theta_num) * S with S = L_0 + L_1 + ... + L_{G-1} summed in that
+ * order, each product rounded once in float64; theta_den == 0 disables it.  Ties of the least-loaded
+ * choice go to the lowest GPU number.  Outputs as in oracle_score.
+ */
+int oracle_score_online(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
+                        int32_t n_experts, const int64_t* fam_off, int32_t n_fam, const int32_t* home_start,
+                        const int32_t* home_size, int32_t n_gpus, int32_t n_place, int32_t p_begin, int32_t p_end,
+                        const uint8_t* primary, const uint8_t* secondary, int32_t n_sec, double rho,
+                        int32_t theta_num, int32_t theta_den, const double* state_in, double* state_out,
+                        int64_t* cost_home, int64_t* cost_span, int64_t* load, int64_t* cost_home_fam)
+{
+    const int32_t E = n_experts, k = top_k, G = n_gpus, L = n_layers, R = n_sec;
+    int err = 0;
+    if (G < 1 || G > 32 || k < 1 || k > 16 || k > E || E > 256 || R < 0 || R > 4 || n_fam < 1 || n_fam > 64 ||
+        p_begin < 0 || p_end > n_place || p_begin > p_end) return ORC_ERR_ARG;
+    if (R > 0 && secondary == NULL) return ORC_ERR_ARG;
+    if (!(rho >= 0.0 && rho < 1.0)) return ORC_ERR_ARG;
+    if (fam_off[0] != 0 || fam_off[n_fam] != n_tokens) return ORC_ERR_ARG;
+    for (int32_t f = 0; f < n_fam; ++f) {
+        if (fam_off[f + 1] < fam_off[f]) return ORC_ERR_ARG;
+        if (home_size[f] < 1 || home_start[f] < 0 || home_start[f] + home_size[f] > G) return ORC_ERR_ARG;
+    }
+    for (int32_t p = p_begin; p < p_end; ++p) {
+        cost_home[p] = 0;
+        cost_span[p] = 0;
+        if (cost_home_fam)
+            for (int32_t f = 0; f < n_fam; ++f) cost_home_fam[(int64_t)p * n_fam + f] = 0;
+    }
+    const double gden = (double)theta_den * (double)G, rnum = (double)theta_den + (double)theta_num;
+    const int64_t n_pl = (int64_t)(p_end - p_begin) * L;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
+    for (int64_t job = 0; job < n_pl; ++job) {
+        const int32_t p = p_begin + (int32_t)(job / L), l = (int32_t)(job % L);
+        const uint8_t* prim = primary + ((int64_t)p * L + l) * E;
+        const uint8_t* sec = R > 0 ? secondary + (((int64_t)p * L + l) * E) * R : NULL;
+        int64_t* ld = load + ((int64_t)p * L + l) * G;
+        double Lm[32];
+        for (int32_t m = 0; m < G; ++m) {
+            ld[m] = 0;
+            Lm[m] = state_in ? state_in[((int64_t)p * L + l) * G + m] : 0.0;
+        }
+        /* candidate set C_{l,e} of eq. candidate-set */
+        int n_cand[256], cand[256][5];
+        for (int32_t e = 0; e < E; ++e) {
+            n_cand[e] = 0;
+            if (prim[e] >= G) { err |= ORC_ERR_TABLE; cand[e][n_cand[e]++] = 0; }
+            else cand[e][n_cand[e]++] = prim[e];
+            for (int32_t r = 0; r < R; ++r) {
+                uint8_t g = sec[(int64_t)e * R + r];
+                if (g == ORC_NONE) continue;
+                if (g >= G) { err |= ORC_ERR_TABLE; continue; }
+                int dup = 0;
+                for (int c = 0; c < n_cand[e]; ++c) dup |= cand[e][c] == g;
+                if (dup) { err |= ORC_ERR_TABLE; continue; }
+                cand[e][n_cand[e]++] = g;
+            }
+        }
+
+        int64_t home_acc = 0, span_acc = 0;
+        int64_t fam_acc[64];
+        for (int32_t f = 0; f < n_fam && f < 64; ++f) fam_acc[f] = 0;
+        for (int32_t f = 0; f < n_fam; ++f) {
+            for (int64_t t = fam_off[f]; t < fam_off[f + 1]; ++t) {
+                const int16_t* ids = trace + ((int64_t)l * n_tokens + t) * k;
+                int te = token_error(ids, k, E);
+                if (te) { err |= te; continue; }
+                const int32_t h = home_start[f] + (int32_t)((t - fam_off[f]) % home_size[f]);
+                /* feasible GPUs under the current loads (eq. feasible-set) */
+                int feas[32];
+                if (theta_den == 0) {
+                    for (int32_t m = 0; m < G; ++m) feas[m] = 1;
+                } else {
+                    double S = 0.0;
+                    for (int32_t m = 0; m < G; ++m) S += Lm[m];
+                    const double rhs = rnum * S;
+                    for (int32_t m = 0; m < G; ++m) feas[m] = gden * Lm[m] <= rhs;
+                }
+                int in_r[32], slot_gpu[16];
+                for (int32_t m = 0; m < G; ++m) in_r[m] = 0;
+                for (int32_t s = 0; s < k; ++s) {
+                    int e = ids[s];
+                    if (n_cand[e] == 1) { slot_gpu[s] = cand[e][0]; in_r[cand[e][0]] = 1; }
+                    else slot_gpu[s] = -1;
+                }
+                for (int32_t s = 0; s < k; ++s) {
+                    if (slot_gpu[s] >= 0) continue;
+                    int e = ids[s], pick = -1;
+                    int fc[32], any = 0;
+                    for (int32_t m = 0; m < G; ++m) fc[m] = 0;
+                    for (int c = 0; c < n_cand[e]; ++c)
+                        if (feas[cand[e][c]]) { fc[cand[e][c]] = 1; any = 1; }
+                    if (!any)
+                        for (int c = 0; c < n_cand[e]; ++c) fc[cand[e][c]] = 1;
+                    for (int32_t m = 0; m < G && pick < 0; ++m)
+                        if (fc[m] && in_r[m]) pick = m;
+                    if (pick < 0 && fc[h]) pick = h;
+                    if (pick < 0)
+                        for (int32_t m = 0; m < G; ++m)
+                            if (fc[m] && (pick < 0 || Lm[m] < Lm[pick])) pick = m;
+                    slot_gpu[s] = pick;
+                    in_r[pick] = 1;
+                }
+                int n_cards = 0;
+                for (int32_t m = 0; m < G; ++m) n_cards += in_r[m];
+                int64_t home_cost = n_cards - in_r[h];
+                home_acc += home_cost;
+                span_acc += n_cards - 1;
+                if (f < 64) fam_acc[f] += home_cost;
+                int delta[32];
+                for (int32_t m = 0; m < G; ++m) delta[m] = 0;
+                for (int32_t s = 0; s < k; ++s) { ld[slot_gpu[s]] += 1; delta[slot_gpu[s]] += 1; }
+                /* eq. load-update, after the token's dispatch */
+                for (int32_t m = 0; m < G; ++m) Lm[m] = fma(rho, Lm[m], (double)delta[m]);
+            }
+        }
+        if (state_out)
+            for (int32_t m = 0; m < G; ++m) state_out[((int64_t)p * L + l) * G + m] = Lm[m];
 #pragma omp atomic
         cost_home[p] += home_acc;
 #pragma omp atomic

@@ -350,3 +350,54 @@ def test_tacg_placement_scored(name, setidx):
     np.testing.assert_array_equal(_u32(out["load"]), ro["load"])
     # the grouped placement co-locates the planted clusters: fewer GPUs spanned than the default
     assert ro["cost_span"][1] < ro["cost_span"][0]
+
+
+# ------------------------------------------------------------------------------------------------
+# scoring on uniformly random traces: top-k widths with packed ids of 1-4 words, every replicated
+# slot of a token resolved (tokens with more replicated slots than the per-token word holds), empty
+# families, empty traces
+# ------------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("E,k,L,counts,G,cap,n_rep,R,P,seed", [
+    (16, 8, 2, [700, 0, 513], 4, 4, 16, 2, 20, 1),       # every expert replicated: all slots resolved
+    (16, 16, 1, [300, 301], 8, 2, 16, 3, 9, 2),         # k = 16: two replica indices per token word
+    (64, 16, 2, [1000, 999], 8, 8, 12, 1, 131, 3),
+    (256, 16, 1, [900, 77], 32, 8, 16, 4, 130, 4),      # maximum k, G, R and replicated experts
+    (40, 1, 2, [500, 500, 1], 5, 8, 6, 2, 33, 5),       # k = 1
+    (200, 3, 2, [1200, 3], 25, 8, 10, 2, 129, 6),       # odd k, E > 64
+    (60, 5, 2, [800, 801], 6, 10, 4, 2, 257, 7),        # odd k, E <= 64 (four placements per lane)
+])
+def test_eval_random_shapes(E, k, L, counts, G, cap, n_rep, R, P, seed):
+    _say(f"eval random E={E} k={k} L={L} counts={counts} G={G} R={R} P={P}")
+    off = synth.fam_offsets(counts)
+    F = len(counts)
+    tr = _rand_trace(L, int(off[-1]), k, E, seed)
+    prim = synth.random_placements(P, L, E, G, cap, seed + 100)
+    rng = np.random.default_rng(seed)
+    rep = np.stack([np.sort(rng.choice(E, n_rep, replace=False)) for _ in range(L)])
+    sec = synth.random_secondaries(prim, G, rep, R, seed + 200)
+    hs, hz = synth.home_bands(F, G)
+    Do, _, _ = oracle.coact(tr.cpu(), off, E)
+    ref_o = oracle.placement_load(Do, prim, G)
+    ro = oracle.score(tr.cpu(), off, E, hs, hz, G, prim, sec, ref_o, (3, 20))
+    assert ro["err"] == 0
+    prim_t, sec_t = torch.as_tensor(prim).cuda(), torch.as_tensor(sec).cuda()
+    D, _, e1 = tacg.coact_build(tr, off, E)
+    ref_g = tacg.placement_load(D, prim_t, G, err=e1)
+    out = tacg.eval_placements(tr, off, E, hs, hz, G, prim_t, sec_t, ref_g, theta=(3, 20))
+    assert _err(out["err"]) == 0 and _err(e1) == 0
+    np.testing.assert_array_equal(ref_g.cpu().numpy(), ref_o)
+    np.testing.assert_array_equal(out["cost_home"].cpu().numpy(), ro["cost_home"])
+    np.testing.assert_array_equal(out["cost_span"].cpu().numpy(), ro["cost_span"])
+    np.testing.assert_array_equal(_u32(out["load"]), ro["load"])
+    np.testing.assert_array_equal(out["cost_home_fam"].cpu().numpy(), ro["cost_home_fam"])
+
+
+def test_eval_empty_trace():
+    E, k, L, G, F = 32, 4, 2, 4, 3
+    tr = torch.zeros((L, 0, k), dtype=torch.int16, device="cuda")
+    prim = torch.as_tensor(synth.random_placements(5, L, E, G, 8, 1)).cuda()
+    hs, hz = synth.home_bands(F, G)
+    out = tacg.eval_placements(tr, synth.fam_offsets([0] * F), E, hs, hz, G, prim)
+    assert _err(out["err"]) == 0
+    assert int(out["cost_home"].abs().sum()) == 0 and int(out["cost_span"].abs().sum()) == 0
+    assert int(out["load"].abs().sum()) == 0
