@@ -14,6 +14,13 @@
  *   oracle_score          -- per placement: cross-GPU cost, GESR candidate choice and per-GPU loads
  *                            (Sec. 3.4 eqs. mean-load, feasible-set and the fallback after it; the
  *                            per-token dispatch sets of App. C; the dispatch loads of App. H).
+ *   oracle_score_online   -- the same with the guard and the least-loaded choice reading decayed
+ *                            per-GPU loads updated after every token (Sec. 3.4 eq. load-update).
+ *
+ * Parity unpinned: the order of preference among several feasible candidates (below) is a reading
+ * of Sec. 3.4, which names the ingredients (reached GPUs, the anchor, the loads) but not a rule; the
+ * tests pin this implementation of the reading with hand-built cases and independent brute force,
+ * not with values printed in the paper.
  *
  * Readings taken where the paper is silent (each also used by the HIP path, written separately):
  *   - a token whose ids repeat or fall outside [0, E) is an input error: it is flagged and skipped;
