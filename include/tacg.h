@@ -143,6 +143,31 @@ size_t tacg_eval_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t n_e
                                  int32_t n_place, int32_t n_fam);
 
 /*
+ * Placement scoring with decayed per-GPU loads: the sequential form of the serving rule of Sec. 3.4
+ * (eqs. mean-load, feasible-set and load-update).  Same choice rule, costs and loads as
+ * tacg_eval_placements, but every (placement p, layer l) keeps its own loads L_m, which the guard and
+ * the least-loaded choice read, and which are updated after every token in trace order:
+ *   L_m <- fma(rho, L_m, Delta_m)        (float64, one rounding; Delta_m = the token's slots on m)
+ *   feasible: theta_den * G * L_m <= (theta_den + theta_num) * S,  S = L_0 + ... + L_{G-1} in that
+ *   order, each product rounded once (theta_den == 0: all feasible).
+ * state_in_or_null: float64 [P][L][G] initial loads (NULL = zero); state_out_or_null: the loads
+ * after the last token (may be the same buffer as state_in, so that a trace can be scored in token
+ * chunks: the costs and loads of the chunks add up to those of the whole trace when every chunk keeps
+ * each family's anchor phase).  0 <= rho < 1.  Tables and outputs as in tacg_eval_placements; no
+ * workspace and no limit on the number of replicated experts.  One wave scans 64 placements of one
+ * layer, so the time grows with N and the parallelism is P * L lanes.
+ * Data errors: TACG_ERR_ID_RANGE / _DUP (the token-layer is not served and does not update the
+ * loads), TACG_ERR_TABLE.  flags: must be 0.
+ */
+int tacg_eval_online(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+                     const int64_t* fam_off_host, int32_t n_fam, const int32_t* home_start_host,
+                     const int32_t* home_size_host, int32_t n_gpus, int32_t n_place, const uint8_t* primary,
+                     const uint8_t* secondary_or_null, int32_t n_sec, double rho, int32_t theta_num,
+                     int32_t theta_den, const double* state_in_or_null, double* state_out_or_null,
+                     uint64_t* cost_home, uint64_t* cost_span, uint32_t* load, uint64_t* cost_home_fam_or_null,
+                     uint32_t flags, uint32_t* d_err, void* hip_stream);
+
+/*
  * Jain's fairness index and MaxVio of per-GPU loads (App. H eqs. jain and maxvio):
  *   Jain = (sum_m L_m)^2 / (G sum_m L_m^2),  MaxVio = (max_m L_m - mean) / mean.
  * per_layer = 0: L_m = sum_l load[p][l][m], outputs float jain[P], maxvio[P];

@@ -64,6 +64,8 @@ def lib():
                                                P, P, P, P, u32, P, P, sz, P]
             L.tacg_eval_workspace_bytes.argtypes = [i64, i32, i32, i32, i32, i32]
             L.tacg_eval_workspace_bytes.restype = sz
+            L.tacg_eval_online.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, P, P, i32, f64, i32, i32,
+                                           P, P, P, P, P, P, u32, P, P]
             L.tacg_jain.argtypes = [P, i32, i32, i32, i32, P, P, P]
             L.tacg_strerror.argtypes = [ctypes.c_int]
             L.tacg_strerror.restype = ctypes.c_char_p
@@ -204,6 +206,40 @@ def eval_placements(trace: torch.Tensor, fam_off, n_experts: int, home_start, ho
         _dptr(out["cost_home"]), _dptr(out["cost_span"]), _dptr(out["load"]), _dptr(out["cost_home_fam"]), 0,
         _dptr(err), _dptr(ws), ws.numel(), _stream(stream))
     _check("tacg_eval_placements", st)
+    out["err"] = err
+    return out
+
+
+def eval_online(trace: torch.Tensor, fam_off, n_experts: int, home_start, home_size, n_gpus: int,
+                primary: torch.Tensor, secondary: Optional[torch.Tensor] = None, rho: float = 0.995, theta=(3, 20),
+                state: Optional[torch.Tensor] = None, want_state: bool = True, want_fam: bool = True,
+                err: Optional[torch.Tensor] = None, out: Optional[dict] = None, stream=None) -> dict:
+    """Scoring with decayed per-GPU loads (tacg_eval_online).  state: float64 [P][L][G] initial loads
+    or None (zero).  dict(cost_home, cost_span, load, cost_home_fam, state (final loads), err)."""
+    L_, N, k = trace.shape
+    off = _host_i64(fam_off)
+    F = off.size - 1
+    hs, hz = _host_i32(home_start), _host_i32(home_size)
+    P = primary.shape[0]
+    dev = trace.device
+    R = 0 if secondary is None else int(secondary.shape[-1])
+    if out is None:
+        out = dict(cost_home=torch.empty(P, dtype=torch.int64, device=dev),
+                   cost_span=torch.empty(P, dtype=torch.int64, device=dev),
+                   load=torch.empty((P, L_, n_gpus), dtype=torch.int32, device=dev),
+                   cost_home_fam=torch.empty((P, F), dtype=torch.int64, device=dev) if want_fam else None,
+                   state=torch.empty((P, L_, n_gpus), dtype=torch.float64, device=dev) if want_state else None)
+    if state is not None and (state.dtype != torch.float64 or tuple(state.shape) != (P, L_, n_gpus)):
+        raise ValueError("state must be float64 [P][L][G]")
+    if err is None:
+        err = _err_tensor(dev)
+    tn, td = theta if theta is not None else (0, 0)
+    st = lib().tacg_eval_online(
+        _dptr(trace), N, L_, k, n_experts, _hptr(off), F, _hptr(hs), _hptr(hz), n_gpus, P, _dptr(primary),
+        _dptr(secondary) if R > 0 else None, R, float(rho), int(tn), int(td), _dptr(state), _dptr(out.get("state")),
+        _dptr(out["cost_home"]), _dptr(out["cost_span"]), _dptr(out["load"]), _dptr(out["cost_home_fam"]), 0,
+        _dptr(err), _stream(stream))
+    _check("tacg_eval_online", st)
     out["err"] = err
     return out
 

@@ -117,6 +117,34 @@ int tacg_eval_placements(const int16_t* trace, int64_t n_tokens, int32_t n_layer
                            as_stream(hip_stream));
 }
 
+int tacg_eval_online(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+                     const int64_t* fam_off_host, int32_t n_fam, const int32_t* home_start_host,
+                     const int32_t* home_size_host, int32_t n_gpus, int32_t n_place, const uint8_t* primary,
+                     const uint8_t* secondary_or_null, int32_t n_sec, double rho, int32_t theta_num,
+                     int32_t theta_den, const double* state_in_or_null, double* state_out_or_null,
+                     uint64_t* cost_home, uint64_t* cost_span, uint32_t* load, uint64_t* cost_home_fam_or_null,
+                     uint32_t flags, uint32_t* d_err, void* hip_stream) {
+  int rc = check_trace(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam);
+  if (rc != TACG_OK) return rc;
+  if (flags != 0) return TACG_E_INVAL;
+  if (n_gpus < 1 || n_place < 1 || n_sec < 0) return TACG_E_INVAL;
+  if (n_gpus > TACG_MAX_GPUS || n_sec > TACG_MAX_SECONDARY) return TACG_E_UNSUPPORTED;
+  if (primary == nullptr || cost_home == nullptr || cost_span == nullptr || load == nullptr || d_err == nullptr)
+    return TACG_E_INVAL;
+  if (n_sec > 0 && secondary_or_null == nullptr) return TACG_E_INVAL;
+  if (!(rho >= 0.0 && rho < 1.0)) return TACG_E_INVAL;
+  if (theta_num < 0 || theta_den < 0 || theta_num > (1 << 20) || theta_den > (1 << 20)) return TACG_E_INVAL;
+  if (home_start_host == nullptr || home_size_host == nullptr) return TACG_E_INVAL;
+  for (int f = 0; f < n_fam; ++f) {
+    if (home_size_host[f] < 1 || home_start_host[f] < 0 || home_start_host[f] + home_size_host[f] > n_gpus)
+      return TACG_E_INVAL;
+  }
+  return tacg::launch_eval_online(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, home_start_host,
+                                  home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec, rho, theta_num,
+                                  theta_den, state_in_or_null, state_out_or_null, cost_home, cost_span, load,
+                                  cost_home_fam_or_null, d_err, as_stream(hip_stream));
+}
+
 int tacg_jain(const uint32_t* load, int32_t n_place, int32_t n_layers, int32_t n_gpus, int32_t per_layer,
               float* jain, float* maxvio, void* hip_stream) {
   if (load == nullptr || jain == nullptr || maxvio == nullptr) return TACG_E_INVAL;

@@ -48,6 +48,12 @@ int launch_eval(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_
                 const uint8_t* secondary, int32_t n_sec, const int64_t* load_ref, int32_t theta_num,
                 int32_t theta_den, uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
                 uint64_t* cost_home_fam, uint32_t* d_err, void* workspace, hipStream_t stream);
+int launch_eval_online(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+                       const int64_t* fam_off_host, int32_t n_fam, const int32_t* home_start_host,
+                       const int32_t* home_size_host, int32_t n_gpus, int32_t n_place, const uint8_t* primary,
+                       const uint8_t* secondary, int32_t n_sec, double rho, int32_t theta_num, int32_t theta_den,
+                       const double* state_in, double* state_out, uint64_t* cost_home, uint64_t* cost_span,
+                       uint32_t* load, uint64_t* cost_home_fam, uint32_t* d_err, hipStream_t stream);
 int launch_placement_load(const uint32_t* D, int32_t n_fam, int32_t n_layers, int32_t n_experts,
                           const uint8_t* primary, int32_t n_place, int32_t n_gpus, int64_t* load_ref,
                           uint32_t* d_err, hipStream_t stream);

@@ -127,6 +127,33 @@ def test_eval_argument_errors(L):
     assert call(off_=np.array([0, 60, 90], dtype=np.int64)) == tacg.E_INVAL
 
 
+def test_eval_online_argument_errors(L):
+    off = np.array([0, 60, 100], dtype=np.int64)
+    hs = np.array([0, 2], dtype=np.int32)
+    hz = np.array([2, 2], dtype=np.int32)
+
+    def call(G=4, P=3, R=0, sec=None, rho=0.995, hs_=hs, hz_=hz, flags=0, tn=3, td=20, off_=off, ch=FAKE):
+        return L.tacg_eval_online(FAKE, 100, 2, 2, 8, off_.ctypes.data_as(ctypes.c_void_p), 2,
+                                  hs_.ctypes.data_as(ctypes.c_void_p), hz_.ctypes.data_as(ctypes.c_void_p),
+                                  G, P, FAKE, sec, R, rho, tn, td, None, None, ch, FAKE, FAKE, None, flags, FAKE,
+                                  None)
+
+    assert call(G=33) == tacg.E_UNSUPPORTED
+    assert call(G=0) == tacg.E_INVAL
+    assert call(P=0) == tacg.E_INVAL
+    assert call(R=5, sec=FAKE) == tacg.E_UNSUPPORTED
+    assert call(R=2, sec=None) == tacg.E_INVAL
+    assert call(rho=1.0) == tacg.E_INVAL
+    assert call(rho=-0.1) == tacg.E_INVAL
+    assert call(rho=float("nan")) == tacg.E_INVAL
+    assert call(hz_=np.array([2, 0], dtype=np.int32)) == tacg.E_INVAL
+    assert call(hs_=np.array([0, 3], dtype=np.int32)) == tacg.E_INVAL
+    assert call(flags=1) == tacg.E_INVAL
+    assert call(td=-1) == tacg.E_INVAL
+    assert call(ch=None) == tacg.E_INVAL
+    assert call(off_=np.array([0, 60, 90], dtype=np.int64)) == tacg.E_INVAL
+
+
 def test_jain_and_load_argument_errors(L):
     assert L.tacg_jain(FAKE, 2, 1, 33, 0, FAKE, FAKE, None) == tacg.E_UNSUPPORTED
     assert L.tacg_jain(FAKE, 2, 1, 4, 2, FAKE, FAKE, None) == tacg.E_INVAL
