@@ -68,6 +68,9 @@ def parse():
     ap.add_argument("--config", default="deepseek_v3")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-quality", action="store_true", help="skip the untimed placement-quality context")
+    ap.add_argument("--no-online", action="store_true", help="skip the decayed-load scoring measurement")
+    ap.add_argument("--online-tokens", type=int, default=1 << 19,
+                    help="serving-trace tokens of the decayed-load scoring sample")
     ap.add_argument("--tokens", type=int, default=0, help="tokens per trace (0 = the preset's; for profiling runs)")
     ap.add_argument("--layers", type=int, default=0, help="MoE layers (0 = the preset's; for profiling runs)")
     ap.add_argument("--cpu-layers", type=int, default=0, help="layers of the oracle's scoring sample (0 = all)")
@@ -268,9 +271,39 @@ def main():
     log(f"timed {args.steps} steps: {wall / args.steps * 1e3:.1f} ms/step")
     if not args.no_quality:
         result["placement_quality"] = placement_quality(w, ps, cfg, D, C, err)
+    if not args.no_online:
+        result["online_scoring"] = online_scoring(w, ps, cfg, prim, sec, err, args.online_tokens)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, ps, cfg, args.cpu_layers)
     print(json.dumps(result), flush=True)
+
+
+def online_scoring(w, ps, cfg, prim, sec, err, n_tokens, reps=3):
+    """Untimed by the step: tacg_eval_online (decayed per-GPU loads, rho = 0.995, theta = 3/20) over
+    the first tokens of the serving trace (one family mix prefix), every placement and layer."""
+    import numpy as np
+    import torch
+
+    import paper_2606_01007_amd as tacg
+
+    n = min(n_tokens, w.trace_serve.shape[1])
+    tr = w.trace_serve[:, :n].contiguous()
+    off = np.minimum(np.asarray(w.fam_off_serve, dtype=np.int64), n)
+    out = None
+    t = []
+    for _ in range(reps + 1):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        out = tacg.eval_online(tr, off, cfg.E, ps["home_start"], ps["home_size"], ps["n_gpus"], prim, sec,
+                               rho=0.995, theta=(3, 20), err=err, out=out)
+        b.record()
+        torch.cuda.synchronize()
+        t.append(a.elapsed_time(b) * 1e-3)
+    sec_per = float(np.mean(t[1:]))
+    P, L = prim.shape[0], tr.shape[0]
+    return {"value": P * n / sec_per, "unit": "placements×tokens/s", "ms": sec_per * 1e3,
+            "placement_token_layers_per_s": P * n * L / sec_per,
+            "sample": f"first {n} tokens of the serving trace, {P} placements x {L} layers, rho=0.995, theta=3/20"}
 
 
 def placement_quality(w, ps, cfg, D, C, err):

@@ -7,10 +7,11 @@
 //
 // Kernel design (gfx950): the scan over tokens is sequential, the (placement, layer) scans are
 // independent.  Lane = placement, wave = 64 placements of one layer, one wave per workgroup.
-//   * LDS holds, for the wave's placements, the candidate mask of every expert (cm[e][lane]: one bit
-//     for an expert served only by its primary, several for a replicated one) and the per-GPU
-//     dispatch counters of every lane (cnt[m][lane]; a lane owns its column, so the adds never
-//     collide between lanes).
+//   * LDS holds, for the wave's placements, every expert's primary GPU (pg[e][lane], one byte), the
+//     candidate masks of the experts that have a secondary in any of these placements (rm[r][lane],
+//     up to kRepLds of them; rix[e] maps an expert to its row, and the rare experts beyond that
+//     read their tables from memory), and per-lane dispatch counters (cnt[m][lane]).  About 36 KB at
+//     E = 256, so four waves share a CU and all P * L / 64 waves are resident at once.
 //   * The wave loads 64 token-layers at once (one per lane), packs their ids and a word with the
 //     validity, family and anchor position, and broadcasts them token by token with v_readlane.
 //   * The loads live in 32 float64 registers per lane.  The per-token dispatch counts Delta are kept
@@ -23,6 +24,8 @@ namespace {
 
 constexpr int kLanes = 64;
 constexpr uint8_t kNone = 0xFF;
+constexpr uint8_t kOver = 0xFE;  // replicated expert without an LDS row (read from memory)
+constexpr int kRepLds = 48;      // candidate-mask rows in LDS per workgroup
 
 struct OnArgs {
   const int16_t* trace;
@@ -85,6 +88,62 @@ __device__ __forceinline__ uint32_t find_first_bit(uint32_t x) {
   return r;
 }
 
+// Candidate GPUs of one (placement, layer, expert) as a mask: the primary and the valid secondaries.
+// An invalid table (flagged) yields GPU 0 so that every later choice stays in range.
+__device__ __forceinline__ uint32_t candidate_mask(const OnArgs& a, bool live, int64_t pe, uint32_t& err) {
+  uint32_t m = 0;
+  if (live) {
+    const uint8_t g0 = a.primary[pe];
+    if (g0 < a.G) m = 1u << g0;
+    else err |= TACG_ERR_TABLE;
+    for (int r = 0; r < a.R; ++r) {
+      const uint8_t g = a.secondary[pe * a.R + r];
+      if (g == kNone) continue;
+      if (g >= a.G || ((m >> g) & 1u)) {
+        err |= TACG_ERR_TABLE;
+        continue;
+      }
+      m |= 1u << g;
+    }
+  }
+  return m ? m : 1u;
+}
+
+// Candidate mask of expert e for this lane: its LDS row, or the tables themselves for an expert
+// beyond the LDS rows.
+__device__ __forceinline__ uint32_t slot_mask(const OnArgs& a, const uint32_t* rm, const uint8_t* rix, uint32_t e,
+                                              bool live, int64_t base, int lane) {
+  const uint8_t r = rix[e];
+  if (r != kOver) return rm[r * kLanes + lane];
+  uint32_t unused = 0;
+  return candidate_mask(a, live, base + e, unused);
+}
+
+// argmin over the GPUs of fc of the loads, ties to the lowest number, as a balanced tree of pairwise
+// minima (the left, lower-numbered operand wins ties, so the result is the sequential argmin)
+__device__ __forceinline__ uint32_t least_loaded(const double (&Lm)[32], uint32_t fc) {
+  double v[16];
+  uint32_t ix[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const double a0 = ((fc >> (2 * i)) & 1u) ? Lm[2 * i] : __builtin_inf();
+    const double a1 = ((fc >> (2 * i + 1)) & 1u) ? Lm[2 * i + 1] : __builtin_inf();
+    const bool right = a1 < a0;
+    v[i] = right ? a1 : a0;
+    ix[i] = right ? 2u * i + 1u : 2u * i;
+  }
+#pragma unroll
+  for (int w = 8; w >= 1; w >>= 1) {
+#pragma unroll
+    for (int i = 0; i < w; ++i) {
+      const bool right = v[2 * i + 1] < v[2 * i];
+      v[i] = right ? v[2 * i + 1] : v[2 * i];
+      ix[i] = right ? ix[2 * i + 1] : ix[2 * i];
+    }
+  }
+  return ix[0];
+}
+
 // grid (ceil(P / 64), L), 64 threads.
 template <int K>
 __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
@@ -95,32 +154,33 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
   const int p = blockIdx.x * kLanes + lane;
   const bool live = p < a.P;
   const int E = a.E, G = a.G, L = a.L;
-  uint32_t* cm = lds;                      // [E][64] candidate masks
-  uint32_t* cnt = lds + E * kLanes;        // [32][64] dispatch counters
+  uint32_t* rm = lds;                                                  // [kRepLds][64] candidate masks
+  uint32_t* cnt = rm + kRepLds * kLanes;                               // [32][64] dispatch counters
+  uint8_t* pg = reinterpret_cast<uint8_t*>(cnt + 32 * kLanes);          // [E][64] primary GPUs
+  uint8_t* rix = pg + E * kLanes;                                      // [E] row of rm, kNone or kOver
   uint32_t err = 0;
 
-  // ---- candidate masks of this lane's placement (eq. candidate-set) ----
+  // ---- candidate sets of this lane's placement (eq. candidate-set) ----
   const int64_t base = (static_cast<int64_t>(p) * L + l) * E;
+  int nr = 0;  // rows of rm in use (workgroup-uniform)
   for (int e = 0; e < E; ++e) {
-    uint32_t m = 0;
-    if (live) {
-      const uint8_t g0 = a.primary[base + e];
-      if (g0 < G) m = 1u << g0;
-      else err |= TACG_ERR_TABLE;
-      for (int r = 0; r < a.R; ++r) {
-        const uint8_t g = a.secondary[(base + e) * a.R + r];
-        if (g == kNone) continue;
-        if (g >= G || ((m >> g) & 1u)) {
-          err |= TACG_ERR_TABLE;
-          continue;
-        }
-        m |= 1u << g;
+    const uint32_t m = candidate_mask(a, live, base + e, err);
+    pg[e * kLanes + lane] = static_cast<uint8_t>(find_first_bit(m));
+    const bool multi = __popc(m) > 1;
+    uint8_t r = kNone;
+    if (__ballot(multi)) {
+      if (nr < kRepLds) {
+        rm[nr * kLanes + lane] = m;
+        r = static_cast<uint8_t>(nr++);
+      } else {
+        r = kOver;
       }
     }
-    cm[e * kLanes + lane] = m ? m : 1u;  // an invalid table (flagged) keeps every choice in range
+    if (lane == 0) rix[e] = r;
   }
 #pragma unroll
   for (int m = 0; m < 32; ++m) cnt[m * kLanes + lane] = 0;
+  __syncthreads();
 
   double Lm[32];
 #pragma unroll
@@ -153,7 +213,9 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
         ok &= raw[s] < static_cast<uint32_t>(E);
 #pragma unroll
         for (int q = 0; q < s; ++q) dup |= raw[s] == raw[q];
-        pk[s >> 2] |= min(raw[s], static_cast<uint32_t>(E - 1)) << (8 * (s & 3));
+        const uint32_t id = min(raw[s], static_cast<uint32_t>(E - 1));
+        pk[s >> 2] |= id << (8 * (s & 3));
+        if (rix[id] != kNone) info |= 1u << (16 + s);  // an expert with several candidates somewhere
       }
       if (!ok) err |= TACG_ERR_ID_RANGE;
       if (dup) err |= TACG_ERR_ID_DUP;
@@ -162,7 +224,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
       const uint4 fr = a.fam[f];
       const uint32_t hz = (fr.z >> 8) & 0xffu;
       const uint32_t pos = static_cast<uint32_t>((t - static_cast<int64_t>(fr.x)) % hz);
-      info = ((ok && !dup) ? 1u : 0u) | (static_cast<uint32_t>(f) << 1) | (pos << 8);
+      info |= ((ok && !dup) ? 1u : 0u) | (static_cast<uint32_t>(f) << 1) | (pos << 8);
     }
     const int ntile = static_cast<int>(min(static_cast<int64_t>(kLanes), a.N - tile));
     for (int j = 0; j < ntile; ++j) {
@@ -178,7 +240,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
         fam_acc = 0;
         cur_f = f;
       }
-      const uint32_t h = (a.fam[f].z & 0xffu) + (tinfo >> 8);
+      const uint32_t h = (a.fam[f].z & 0xffu) + ((tinfo >> 8) & 0xffu);
 
       // single-candidate slots first: they form the set R of GPUs the token reaches
       Delta<(K > 15)> dl;
@@ -187,15 +249,20 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
 #pragma unroll
       for (int s = 0; s < K; ++s) {
         const uint32_t e = __builtin_amdgcn_ubfe(ids[s >> 2], 8 * (s & 3), 8);
-        const uint32_t c = cm[e * kLanes + lane];
-        if (__popc(c) == 1) {
-          R |= c;
-          const uint32_t g = find_first_bit(c);
-          dl.add(g);
-          cnt[g * kLanes + lane] += 1;
+        uint32_t g;
+        if ((tinfo >> (16 + s)) & 1u) {  // workgroup-uniform: e has several candidates somewhere
+          const uint32_t c = slot_mask(a, rm, rix, e, live, base, lane);
+          if (__popc(c) > 1) {
+            pend |= 1u << s;
+            continue;
+          }
+          g = find_first_bit(c);
         } else {
-          pend |= 1u << s;
+          g = pg[e * kLanes + lane];
         }
+        R |= 1u << g;
+        dl.add(g);
+        __hip_atomic_fetch_add(&cnt[g * kLanes + lane], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
       }
       if (__ballot(pend != 0)) {
         // feasible GPUs under the current loads (eq. feasible-set with the mean of eq. mean-load)
@@ -222,7 +289,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
           if (!((pend >> s) & 1u)) continue;
           const uint64_t wd = s < 8 ? id_lo : id_hi;
           const uint32_t e = static_cast<uint32_t>(wd >> (8 * (s & 7))) & 0xffu;
-          const uint32_t c = cm[e * kLanes + lane];
+          const uint32_t c = slot_mask(a, rm, rix, e, live, base, lane);
           uint32_t fc = c & feas;
           if (!fc) fc = c;
           uint32_t pick;
@@ -231,18 +298,11 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
           } else if ((fc >> h) & 1u) {
             pick = h;
           } else {
-            pick = 32;
-            double best = 0.0;
-#pragma unroll
-            for (int m = 0; m < 32; ++m) {
-              const bool take = ((fc >> m) & 1u) && (pick == 32 || Lm[m] < best);
-              best = take ? Lm[m] : best;
-              pick = take ? static_cast<uint32_t>(m) : pick;
-            }
+            pick = least_loaded(Lm, fc);
           }
           R |= 1u << pick;
           dl.add(pick);
-          cnt[pick * kLanes + lane] += 1;
+          __hip_atomic_fetch_add(&cnt[pick * kLanes + lane], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
       }
       const uint32_t n = __popc(R);
@@ -274,7 +334,8 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
 
 template <int K>
 void launch_on(const OnArgs& a, hipStream_t stream) {
-  const size_t lds = (static_cast<size_t>(a.E) * kLanes + 32 * kLanes) * sizeof(uint32_t);
+  const size_t lds = (static_cast<size_t>(kRepLds) * kLanes + 32 * kLanes) * sizeof(uint32_t) +
+                     static_cast<size_t>(a.E) * kLanes + static_cast<size_t>(a.E);
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&on_main<K>), hipFuncAttributeMaxDynamicSharedMemorySize,
                             static_cast<int>(lds));
   hipLaunchKernelGGL(on_main<K>, dim3((a.P + kLanes - 1) / kLanes, a.L), dim3(kLanes), lds, stream, a);

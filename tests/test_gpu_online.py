@@ -73,6 +73,7 @@ def test_hand_worked_alternation():
     (200, 3, 2, [1200, 3], 25, 8, 10, 2, 65, 0.5, (0, 0), 6),          # guard off
     (60, 5, 2, [800, 801], 6, 10, 4, 2, 64, 0.999, (3, 20), 7),
     (30, 4, 2, [400, 400], 1, 30, 0, 0, 10, 0.995, (3, 20), 8),        # G = 1, no replicas
+    (256, 8, 1, [600, 300], 32, 8, 100, 2, 64, 0.995, (3, 20), 9),     # more replicated experts than LDS rows
 ])
 def test_online_parity(E, k, L, counts, G, cap, n_rep, R, P, rho, theta, seed):
     _say(f"online E={E} k={k} L={L} counts={counts} G={G} R={R} P={P} rho={rho} theta={theta}")
