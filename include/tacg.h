@@ -96,6 +96,19 @@ int tacg_reweight(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t n
 size_t tacg_reweight_workspace_bytes(int32_t n_fam, int32_t n_layers, int32_t n_experts);
 
 /*
+ * Scores that identify generic experts (Sec. 3.4, eq. generic-score), from the counts of
+ * tacg_coact_build, per layer l and expert e, with A_f = C_f / N_f off the diagonal (as in
+ * tacg_reweight) and A-bar = mean_f A_f:
+ *   cent[l][e] = sum_e' A-bar(e, e')                                   (centrality)
+ *   cons[l][e] = mean_f cos(A_f(e, :), A-bar(e, :)), 0 for a zero row  (cross-family consistency)
+ *   spec[l][e] = max_f || A_f(e, :) - A-bar(e, :) ||_2                 (task-specific deviation)
+ * so that r = cent + lambda1 * cons - lambda2 * spec ranks the generic experts of a layer.
+ * Outputs: double [L][E] each; float64 arithmetic, summation order unspecified.  No workspace.
+ */
+int tacg_gesr_scores(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t n_layers, int32_t n_experts,
+                     int32_t top_k, double* cent, double* cons, double* spec, void* hip_stream);
+
+/*
  * Snapshot GPU loads for the serving guard of Sec. 3.4 (eq. mean-load uses per-GPU loads L_m):
  * load_ref[p][l][m] = sum over families f and experts e with primary[p][l][e] == m of D[f][l][e],
  * i.e. the dispatch load of GPU m when every expert is served by its primary GPU.
@@ -166,6 +179,18 @@ int tacg_eval_online(const int16_t* trace, int64_t n_tokens, int32_t n_layers, i
                      int32_t theta_den, const double* state_in_or_null, double* state_out_or_null,
                      uint64_t* cost_home, uint64_t* cost_span, uint32_t* load, uint64_t* cost_home_fam_or_null,
                      uint32_t flags, uint32_t* d_err, void* hip_stream);
+
+/*
+ * Grouping objective of Sec. 3.3 (eq. grouping-objective) for P placements: the within-group affinity
+ *   objective[p][l] = sum over GPUs m of sum over ordered pairs e != e' with primary[p][l][e] ==
+ *                     primary[p][l][e'] == m of a_tilde[l][e][e'],
+ * accumulated in float64 (the order of the additions is unspecified, so the last bits may differ
+ * from a sequential sum).  Inputs: float a_tilde[L][E][E] (tacg_reweight), uint8 primary[P][L][E].
+ * Output: double objective[P][L].  Data errors: TACG_ERR_TABLE (an entry >= G; that expert is left
+ * out of every group).
+ */
+int tacg_group_objective(const float* a_tilde, int32_t n_layers, int32_t n_experts, const uint8_t* primary,
+                         int32_t n_place, int32_t n_gpus, double* objective, uint32_t* d_err, void* hip_stream);
 
 /*
  * Jain's fairness index and MaxVio of per-GPU loads (App. H eqs. jain and maxvio):

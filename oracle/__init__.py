@@ -293,3 +293,62 @@ def comm_reduction(comm_base, comm_method):
     """eq. comm-red, in percent."""
     return (np.asarray(comm_base, dtype=np.float64) - np.asarray(comm_method, dtype=np.float64)) \
         / np.asarray(comm_base, dtype=np.float64) * 100.0
+
+
+# ------------------------------------------------------------------------------------------------
+# grouping objective
+# ------------------------------------------------------------------------------------------------
+def grouping_objective(a_tilde, primary, n_gpus: int):
+    """Within-group affinity of eq. grouping-objective for every placement and layer:
+    obj[p][l] = sum over GPUs m of sum over ordered pairs e != e' both placed on m of a_tilde[l][e][e']
+    (float64; literal loops over the members of each GPU)."""
+    at = np.asarray(a_tilde, dtype=np.float64)
+    prim = np.asarray(primary)
+    P, L, E = prim.shape
+    out = np.zeros((P, L), dtype=np.float64)
+    for p in range(P):
+        for l in range(L):
+            members = [[] for _ in range(n_gpus)]
+            for e in range(E):
+                members[int(prim[p, l, e])].append(e)
+            total = 0.0
+            for m in range(n_gpus):
+                for e in members[m]:
+                    for e2 in members[m]:
+                        if e2 != e:
+                            total += at[l, e, e2]
+            out[p, l] = total
+    return out
+
+
+# ------------------------------------------------------------------------------------------------
+# GESR identification scores
+# ------------------------------------------------------------------------------------------------
+def gesr_scores(D, C, top_k: int):
+    """Centrality, cross-family consistency and task-specific deviation of every expert (Sec. 3.4,
+    eq. generic-score), per layer, in float64:
+      Cent(e) = sum_e' A-bar(e, e'),    A-bar = mean over families of A_f (zero diagonal);
+      Cons(e) = mean over families of cos(A_f(e, :), A-bar(e, :))   (0 when either row is zero);
+      Spec(e) = max over families of || A_f(e, :) - A-bar(e, :) ||_2.
+    Returns cent, cons, spec, each [L][E]."""
+    D = _np(D, np.float64)
+    C = _np(C, np.float64)
+    F, L, E = D.shape
+    cent = np.zeros((L, E))
+    cons = np.zeros((L, E))
+    spec = np.zeros((L, E))
+    for l in range(L):
+        A = layer_terms(D[:, l], C[:, l], top_k, 1.0, 1e-8)["A"]     # [F][E][E], zero diagonal
+        a_bar = A.sum(axis=0) / F
+        for e in range(E):
+            cent[l, e] = a_bar[e].sum()
+            nb = np.sqrt((a_bar[e] ** 2).sum())
+            cs = 0.0
+            worst = 0.0
+            for f in range(F):
+                na = np.sqrt((A[f, e] ** 2).sum())
+                cs += float(A[f, e] @ a_bar[e]) / (na * nb) if na > 0 and nb > 0 else 0.0
+                worst = max(worst, float(np.sqrt(((A[f, e] - a_bar[e]) ** 2).sum())))
+            cons[l, e] = cs / F
+            spec[l, e] = worst
+    return cent, cons, spec

@@ -66,6 +66,8 @@ def lib():
             L.tacg_eval_workspace_bytes.restype = sz
             L.tacg_eval_online.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, P, P, i32, f64, i32, i32,
                                            P, P, P, P, P, P, u32, P, P]
+            L.tacg_gesr_scores.argtypes = [P, P, i32, i32, i32, i32, P, P, P, P]
+            L.tacg_group_objective.argtypes = [P, i32, i32, P, i32, i32, P, P, P]
             L.tacg_jain.argtypes = [P, i32, i32, i32, i32, P, P, P]
             L.tacg_strerror.argtypes = [ctypes.c_int]
             L.tacg_strerror.restype = ctypes.c_char_p
@@ -241,6 +243,32 @@ def eval_online(trace: torch.Tensor, fam_off, n_experts: int, home_start, home_s
         _dptr(err), _stream(stream))
     _check("tacg_eval_online", st)
     out["err"] = err
+    return out
+
+
+def gesr_scores(D: torch.Tensor, C: torch.Tensor, top_k: int, stream=None):
+    """float64 cent, cons, spec [L][E] (tacg_gesr_scores)."""
+    F, L_, E = D.shape
+    cent = torch.empty((L_, E), dtype=torch.float64, device=D.device)
+    cons = torch.empty_like(cent)
+    spec = torch.empty_like(cent)
+    st = lib().tacg_gesr_scores(_dptr(D), _dptr(C), F, L_, E, top_k, _dptr(cent), _dptr(cons), _dptr(spec),
+                                _stream(stream))
+    _check("tacg_gesr_scores", st)
+    return cent, cons, spec
+
+
+def group_objective(a_tilde: torch.Tensor, primary: torch.Tensor, n_gpus: int, err: Optional[torch.Tensor] = None,
+                    stream=None) -> torch.Tensor:
+    """float64 [P][L] within-group affinity of every placement (tacg_group_objective)."""
+    L_, E, _ = a_tilde.shape
+    P = primary.shape[0]
+    out = torch.empty((P, L_), dtype=torch.float64, device=a_tilde.device)
+    if err is None:
+        err = _err_tensor(a_tilde.device)
+    st = lib().tacg_group_objective(_dptr(a_tilde), L_, E, _dptr(primary), P, n_gpus, _dptr(out), _dptr(err),
+                                    _stream(stream))
+    _check("tacg_group_objective", st)
     return out
 
 

@@ -69,6 +69,15 @@ int tacg_reweight(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t n
                                a_hat_or_null, workspace, as_stream(hip_stream));
 }
 
+int tacg_gesr_scores(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t n_layers, int32_t n_experts,
+                     int32_t top_k, double* cent, double* cons, double* spec, void* hip_stream) {
+  if (D == nullptr || C == nullptr || cent == nullptr || cons == nullptr || spec == nullptr) return TACG_E_INVAL;
+  if (n_fam < 1 || n_layers < 1 || n_experts < 1 || top_k < 1 || top_k > n_experts) return TACG_E_INVAL;
+  if (n_experts > TACG_MAX_EXPERTS || n_fam > TACG_MAX_FAMILIES || top_k > TACG_MAX_TOPK) return TACG_E_UNSUPPORTED;
+  if (n_layers > 65535) return TACG_E_UNSUPPORTED;
+  return tacg::launch_gesr_scores(D, C, n_fam, n_layers, n_experts, top_k, cent, cons, spec, as_stream(hip_stream));
+}
+
 int tacg_placement_load(const uint32_t* D, int32_t n_fam, int32_t n_layers, int32_t n_experts,
                         const uint8_t* primary, int32_t n_place, int32_t n_gpus, int64_t* load_ref, uint32_t* d_err,
                         void* hip_stream) {
@@ -143,6 +152,17 @@ int tacg_eval_online(const int16_t* trace, int64_t n_tokens, int32_t n_layers, i
                                   home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec, rho, theta_num,
                                   theta_den, state_in_or_null, state_out_or_null, cost_home, cost_span, load,
                                   cost_home_fam_or_null, d_err, as_stream(hip_stream));
+}
+
+int tacg_group_objective(const float* a_tilde, int32_t n_layers, int32_t n_experts, const uint8_t* primary,
+                         int32_t n_place, int32_t n_gpus, double* objective, uint32_t* d_err, void* hip_stream) {
+  if (a_tilde == nullptr || primary == nullptr || objective == nullptr || d_err == nullptr) return TACG_E_INVAL;
+  if (n_layers < 1 || n_experts < 1 || n_place < 0 || n_gpus < 1) return TACG_E_INVAL;
+  if (n_experts > TACG_MAX_EXPERTS || n_gpus > TACG_MAX_GPUS) return TACG_E_UNSUPPORTED;
+  if (n_place == 0) return TACG_OK;
+  if (n_layers > 65535) return TACG_E_UNSUPPORTED;
+  return tacg::launch_group_objective(a_tilde, n_layers, n_experts, primary, n_place, n_gpus, objective, d_err,
+                                      as_stream(hip_stream));
 }
 
 int tacg_jain(const uint32_t* load, int32_t n_place, int32_t n_layers, int32_t n_gpus, int32_t per_layer,

@@ -193,6 +193,73 @@ __global__ __launch_bounds__(256) void rw_graph(int F, int L, int E, double alph
   }
 }
 
+// GESR identification scores (Sec. 3.4, eq. generic-score) per row i of layer l, float64:
+// Cent = sum_j A-bar(i, j); Cons = mean_f cos(A_f(i, :), A-bar(i, :)) (0 for a zero row);
+// Spec = max_f ||A_f(i, :) - A-bar(i, :)||_2.  One wave per row, lanes over columns; the family rows
+// are read twice (once for A-bar, once for the per-family terms).  grid (L, row blocks), 256 threads.
+__global__ __launch_bounds__(256) void gesr_scores_kernel(const uint32_t* __restrict__ D,
+                                                          const uint32_t* __restrict__ C, int F, int L, int E, int k,
+                                                          double* __restrict__ cent, double* __restrict__ cons,
+                                                          double* __restrict__ spec) {
+  __shared__ double inv_n[TACG_MAX_FAMILIES];
+  const int l = blockIdx.x;
+  if (threadIdx.x < F) {
+    const double n = family_tokens(D, threadIdx.x, l, L, E, k);
+    inv_n[threadIdx.x] = n > 0 ? 1.0 / n : 0.0;
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int r0 = blockIdx.y * kRows, r1 = min(E, r0 + kRows);
+  for (int i = r0 + wave; i < r1; i += nw) {
+    double ab[4] = {0, 0, 0, 0};
+    for (int f = 0; f < F; ++f) {
+      const uint32_t* row = C + ((static_cast<int64_t>(f) * L + l) * E + i) * E;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = lane + 64 * q;
+        if (j < E && j != i) ab[q] += row[j] * inv_n[f];
+      }
+    }
+    double cs = 0.0, nb2 = 0.0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      ab[q] /= F;
+      cs += ab[q];
+      nb2 += ab[q] * ab[q];
+    }
+    cs = wave_sum(cs);
+    nb2 = wave_sum(nb2);
+    const double nb = sqrt(nb2);
+    double cos_sum = 0.0, worst = 0.0;
+    for (int f = 0; f < F; ++f) {
+      const uint32_t* row = C + ((static_cast<int64_t>(f) * L + l) * E + i) * E;
+      double dot = 0.0, na2 = 0.0, dev2 = 0.0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = lane + 64 * q;
+        if (j < E) {
+          const double a = (j != i) ? row[j] * inv_n[f] : 0.0;
+          dot += a * ab[q];
+          na2 += a * a;
+          dev2 += (a - ab[q]) * (a - ab[q]);
+        }
+      }
+      dot = wave_sum(dot);
+      na2 = wave_sum(na2);
+      dev2 = wave_sum(dev2);
+      const double na = sqrt(na2);
+      cos_sum += (na > 0.0 && nb > 0.0) ? dot / (na * nb) : 0.0;
+      worst = fmax(worst, sqrt(dev2));
+    }
+    if (lane == 0) {
+      const int64_t o = static_cast<int64_t>(l) * E + i;
+      cent[o] = cs;
+      cons[o] = cos_sum / F;
+      spec[o] = worst;
+    }
+  }
+}
+
 }  // namespace
 
 size_t reweight_workspace(int32_t F, int32_t L, int32_t E) {
@@ -210,6 +277,13 @@ int launch_reweight(const uint32_t* D, const uint32_t* C, int32_t F, int32_t L, 
   hipLaunchKernelGGL(rw_rows, dim3(L, rb), dim3(256), 0, stream, D, C, F, L, E, k, ws);
   hipLaunchKernelGGL(rw_pref, dim3(L), dim3(256), 0, stream, D, F, L, E, k, tau, eps, pref, ws);
   hipLaunchKernelGGL(rw_graph, dim3(L, rb), dim3(256), 0, stream, F, L, E, alpha, a_tilde, a_hat, ws);
+  return hipGetLastError() == hipSuccess ? TACG_OK : TACG_E_DEVICE;
+}
+
+int launch_gesr_scores(const uint32_t* D, const uint32_t* C, int32_t F, int32_t L, int32_t E, int32_t k, double* cent,
+                       double* cons, double* spec, hipStream_t stream) {
+  hipLaunchKernelGGL(gesr_scores_kernel, dim3(L, (E + kRows - 1) / kRows), dim3(256), 0, stream, D, C, F, L, E, k,
+                     cent, cons, spec);
   return hipGetLastError() == hipSuccess ? TACG_OK : TACG_E_DEVICE;
 }
 

@@ -39,6 +39,9 @@ int launch_reweight(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t
                     int32_t top_k, double alpha, double tau, double eps, float* pref, float* a_tilde,
                     float* a_hat, void* workspace, hipStream_t stream);
 
+int launch_gesr_scores(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t n_layers, int32_t n_experts,
+                       int32_t top_k, double* cent, double* cons, double* spec, hipStream_t stream);
+
 // ---- placement scoring ---------------------------------------------------------------------
 size_t eval_workspace(int64_t n_tokens, int32_t n_layers, int32_t n_experts, int32_t n_gpus, int32_t n_place,
                       int32_t n_fam);
@@ -54,6 +57,8 @@ int launch_eval_online(const int16_t* trace, int64_t n_tokens, int32_t n_layers,
                        const uint8_t* secondary, int32_t n_sec, double rho, int32_t theta_num, int32_t theta_den,
                        const double* state_in, double* state_out, uint64_t* cost_home, uint64_t* cost_span,
                        uint32_t* load, uint64_t* cost_home_fam, uint32_t* d_err, hipStream_t stream);
+int launch_group_objective(const float* a_tilde, int32_t n_layers, int32_t n_experts, const uint8_t* primary,
+                           int32_t n_place, int32_t n_gpus, double* objective, uint32_t* d_err, hipStream_t stream);
 int launch_placement_load(const uint32_t* D, int32_t n_fam, int32_t n_layers, int32_t n_experts,
                           const uint8_t* primary, int32_t n_place, int32_t n_gpus, int64_t* load_ref,
                           uint32_t* d_err, hipStream_t stream);

@@ -154,6 +154,21 @@ def test_eval_online_argument_errors(L):
     assert call(off_=np.array([0, 60, 90], dtype=np.int64)) == tacg.E_INVAL
 
 
+def test_gesr_scores_argument_errors(L):
+    assert L.tacg_gesr_scores(FAKE, FAKE, 2, 2, 300, 2, FAKE, FAKE, FAKE, None) == tacg.E_UNSUPPORTED
+    assert L.tacg_gesr_scores(FAKE, FAKE, 0, 2, 8, 2, FAKE, FAKE, FAKE, None) == tacg.E_INVAL
+    assert L.tacg_gesr_scores(FAKE, FAKE, 2, 2, 8, 9, FAKE, FAKE, FAKE, None) == tacg.E_INVAL
+    assert L.tacg_gesr_scores(None, FAKE, 2, 2, 8, 2, FAKE, FAKE, FAKE, None) == tacg.E_INVAL
+
+
+def test_group_objective_argument_errors(L):
+    assert L.tacg_group_objective(FAKE, 2, 300, FAKE, 3, 4, FAKE, FAKE, None) == tacg.E_UNSUPPORTED
+    assert L.tacg_group_objective(FAKE, 2, 8, FAKE, 3, 40, FAKE, FAKE, None) == tacg.E_UNSUPPORTED
+    assert L.tacg_group_objective(None, 2, 8, FAKE, 3, 4, FAKE, FAKE, None) == tacg.E_INVAL
+    assert L.tacg_group_objective(FAKE, 0, 8, FAKE, 3, 4, FAKE, FAKE, None) == tacg.E_INVAL
+    assert L.tacg_group_objective(FAKE, 2, 8, FAKE, 0, 4, FAKE, FAKE, None) == tacg.OK      # nothing to do
+
+
 def test_jain_and_load_argument_errors(L):
     assert L.tacg_jain(FAKE, 2, 1, 33, 0, FAKE, FAKE, None) == tacg.E_UNSUPPORTED
     assert L.tacg_jain(FAKE, 2, 1, 4, 2, FAKE, FAKE, None) == tacg.E_INVAL

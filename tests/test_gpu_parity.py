@@ -401,3 +401,60 @@ def test_eval_empty_trace():
     assert _err(out["err"]) == 0
     assert int(out["cost_home"].abs().sum()) == 0 and int(out["cost_span"].abs().sum()) == 0
     assert int(out["load"].abs().sum()) == 0
+
+
+# ------------------------------------------------------------------------------------------------
+# grouping objective over many placements
+# ------------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("name,setidx,n_place", [("qwen15", 0, 300), ("qwen15", 1, 70), ("deepseek16b", 0, 130),
+                                                 ("deepseek_v3", 0, 65)])
+def test_group_objective_parity(name, setidx, n_place):
+    cfg = synth.CONFIGS[name]
+    _say(f"group objective {name} set {setidx} P={n_place}")
+    w = synth.make_workload(name, n_tokens=cfg.F * 500, layers=3, n_place=n_place)
+    ps = w.placement_sets[setidx]
+    Do, Co, _ = oracle.coact(w.trace_group, w.fam_off_group, cfg.E)
+    _, ato, _ = oracle.reweight(Do, Co, cfg.k)
+    at32 = ato.astype(np.float32)                      # the device input precision, used by both sides
+    got = tacg.group_objective(torch.as_tensor(at32).cuda(), torch.as_tensor(ps["primary"]).cuda(), ps["n_gpus"])
+    ref = oracle.grouping_objective(at32.astype(np.float64), ps["primary"], ps["n_gpus"])
+    np.testing.assert_allclose(got.cpu().numpy(), ref, rtol=1e-12, atol=1e-300)
+
+
+def test_group_objective_table_error():
+    at = torch.zeros((1, 8, 8), dtype=torch.float32, device="cuda")
+    prim = torch.zeros((2, 1, 8), dtype=torch.uint8, device="cuda")
+    prim[1, 0, 3] = 7
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    tacg.group_objective(at, prim, 4, err=err)
+    assert _err(err) & tacg.ERR_TABLE
+
+
+# ------------------------------------------------------------------------------------------------
+# GESR identification scores
+# ------------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["tiny", "deepseek16b", "qwen15", "qwen3_30b", "deepseek_v3"])
+def test_gesr_scores_parity(name):
+    cfg = synth.CONFIGS[name]
+    _say(f"gesr scores {name}")
+    n = cfg.tokens_group if name == "tiny" else cfg.F * 700 + 3
+    w = synth.make_workload(name, n_tokens=n, layers=min(cfg.L, 2), n_place=2)
+    D, C, err = tacg.coact_build(w.trace_group.cuda(), w.fam_off_group, cfg.E)
+    cent, cons, spec = tacg.gesr_scores(D, C, cfg.k)
+    assert _err(err) == 0
+    Do, Co, _ = oracle.coact(w.trace_group, w.fam_off_group, cfg.E)
+    co, so, po = oracle.gesr_scores(Do, Co, cfg.k)
+    np.testing.assert_allclose(cent.cpu().numpy(), co, rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(cons.cpu().numpy(), so, rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(spec.cpu().numpy(), po, rtol=1e-12, atol=1e-15)
+
+
+def test_gesr_scores_empty_family():
+    off = [0, 500, 500, 900]
+    tr = _rand_trace(1, 900, 3, 20, 11)
+    D, C, _ = tacg.coact_build(tr, off, 20)
+    cent, cons, spec = tacg.gesr_scores(D, C, 3)
+    Do, Co, _ = oracle.coact(tr.cpu(), off, 20)
+    co, so, po = oracle.gesr_scores(Do, Co, 3)
+    np.testing.assert_allclose(cons.cpu().numpy(), so, rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(spec.cpu().numpy(), po, rtol=1e-12, atol=1e-15)
