@@ -269,6 +269,7 @@ def main():
     }
 
     log(f"timed {args.steps} steps: {wall / args.steps * 1e3:.1f} ms/step")
+    result["aux_ms"] = aux_timings(D, C, prim, cfg, G)
     if not args.no_quality:
         result["placement_quality"] = placement_quality(w, ps, cfg, D, C, err)
     if not args.no_online:
@@ -276,6 +277,33 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, ps, cfg, args.cpu_layers)
     print(json.dumps(result), flush=True)
+
+
+def aux_timings(D, C, prim, cfg, G, reps=5):
+    """Untimed by the step: the host-input helpers on the grouping trace's counts (GESR
+    identification scores) and on the timed placements (grouping objective of every placement)."""
+    import torch
+
+    import paper_2606_01007_amd as tacg
+
+    _, at, _ = tacg.reweight(D, C, cfg.k)
+
+    def timed(fn):
+        fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    return {"gesr_scores": timed(lambda: tacg.gesr_scores(D, C, cfg.k)),
+            "group_objective": timed(lambda: tacg.group_objective(at, prim, G)),
+            "activation_distance": timed(lambda: tacg.activation_distance(D, cfg.k)),
+            "pair_jaccard_top64": timed(lambda: tacg.pair_jaccard(C, 64)),
+            "note": "gesr_scores, activation_distance and pair_jaccard over the grouping counts; "
+                    "group_objective of all placements x layers"}
 
 
 def online_scoring(w, ps, cfg, prim, sec, err, n_tokens, reps=3):

@@ -55,6 +55,7 @@ extern "C" {
 #define TACG_MAX_GPUS 32
 #define TACG_MAX_SECONDARY 4
 #define TACG_MAX_REPLICATED 16
+#define TACG_MAX_TOP_PAIRS 4096
 
 /*
  * Dispatch and co-activation counts per task family and layer (Sec. 3.3, "Scoring task-family
@@ -107,6 +108,25 @@ size_t tacg_reweight_workspace_bytes(int32_t n_fam, int32_t n_layers, int32_t n_
  */
 int tacg_gesr_scores(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t n_layers, int32_t n_experts,
                      int32_t top_k, double* cent, double* cons, double* spec, void* hip_stream);
+
+/*
+ * Motivation diagnostics of App. H (auxiliary metrics), from the counts of tacg_coact_build.
+ *
+ * tacg_activation_distance: the Frobenius distance between the expert-activation distributions of
+ * every two families,  P_f[l][e] = D[f][l][e] / N_{f,l}  (N_{f,l} = sum_e D[f][l][e] / k; P = 0 for an
+ * empty family),  dist[i][j] = || P_i - P_j ||_F  over all layers and experts.  Output: double
+ * dist[F][F] (float64, summation order unspecified).
+ *
+ * tacg_pair_jaccard: per family and layer, the top_n most frequently co-activated pairs e < e' with
+ * a positive count (by count, descending; ties by pair index e * E + e', ascending), written to
+ * int32 top_pairs[F][L][top_n] in increasing pair index and padded with -1; then per layer the
+ * Jaccard overlap |T_i & T_j| / |T_i | T_j| of every two families (1 when both sets are empty),
+ * double jaccard[L][F][F].  1 <= top_n <= TACG_MAX_TOP_PAIRS (the paper uses 64); 2 <= E.
+ */
+int tacg_activation_distance(const uint32_t* D, int32_t n_fam, int32_t n_layers, int32_t n_experts, int32_t top_k,
+                             double* dist, void* hip_stream);
+int tacg_pair_jaccard(const uint32_t* C, int32_t n_fam, int32_t n_layers, int32_t n_experts, int32_t top_n,
+                      int32_t* top_pairs, double* jaccard, void* hip_stream);
 
 /*
  * Snapshot GPU loads for the serving guard of Sec. 3.4 (eq. mean-load uses per-GPU loads L_m):

@@ -352,3 +352,61 @@ def gesr_scores(D, C, top_k: int):
             cons[l, e] = cs / F
             spec[l, e] = worst
     return cent, cons, spec
+
+
+# ------------------------------------------------------------------------------------------------
+# motivation diagnostics
+# ------------------------------------------------------------------------------------------------
+def activation_distance(D, top_k: int):
+    """Frobenius distance between the expert-activation distributions of every two families
+    (App. H, auxiliary motivation metrics): P_f[l][e] = D_f[l][e] / N_{f,l} (the probability that a
+    token of family f activates expert e at layer l; 0 for an empty family), dist[i][j] = ||P_i - P_j||_F
+    over all layers and experts.  float64 [F][F]."""
+    D = _np(D, np.float64)
+    F, L, E = D.shape
+    Pm = np.zeros((F, L, E))
+    for f in range(F):
+        for l in range(L):
+            n = D[f, l].sum() / top_k
+            if n > 0:
+                Pm[f, l] = D[f, l] / n
+    dist = np.zeros((F, F))
+    for i in range(F):
+        for j in range(F):
+            dist[i, j] = np.sqrt(((Pm[i] - Pm[j]) ** 2).sum())
+    return dist
+
+
+def top_pairs(C, top_n: int = 64):
+    """The top_n most frequently co-activated expert pairs of every family and layer: pairs e < e'
+    with a positive count, by count (descending), ties by pair index e * E + e' (ascending); the set
+    listed in increasing pair index, padded with -1.  int64 [F][L][top_n]."""
+    C = _np(C, np.int64)
+    F, L, E, _ = C.shape
+    out = np.full((F, L, top_n), -1, dtype=np.int64)
+    iu, ju = np.triu_indices(E, k=1)
+    idx = iu * E + ju
+    for f in range(F):
+        for l in range(L):
+            cnt = C[f, l][iu, ju]
+            keep = cnt > 0
+            order = np.lexsort((idx[keep], -cnt[keep]))[:top_n]
+            sel = np.sort(idx[keep][order])
+            out[f, l, :sel.size] = sel
+    return out
+
+
+def pair_jaccard(C, top_n: int = 64):
+    """Jaccard overlap of the top_n co-activated pair sets of every two families, per layer
+    (App. H): |T_i & T_j| / |T_i | T_j| (1 when both sets are empty).  float64 [L][F][F]."""
+    T = top_pairs(C, top_n)
+    F, L, _ = T.shape
+    out = np.zeros((L, F, F))
+    for l in range(L):
+        for i in range(F):
+            a = set(int(x) for x in T[i, l] if x >= 0)
+            for j in range(F):
+                b = set(int(x) for x in T[j, l] if x >= 0)
+                u = len(a | b)
+                out[l, i, j] = len(a & b) / u if u else 1.0
+    return out

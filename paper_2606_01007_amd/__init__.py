@@ -66,6 +66,8 @@ def lib():
             L.tacg_eval_workspace_bytes.restype = sz
             L.tacg_eval_online.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, P, P, i32, f64, i32, i32,
                                            P, P, P, P, P, P, u32, P, P]
+            L.tacg_activation_distance.argtypes = [P, i32, i32, i32, i32, P, P]
+            L.tacg_pair_jaccard.argtypes = [P, i32, i32, i32, i32, P, P, P]
             L.tacg_gesr_scores.argtypes = [P, P, i32, i32, i32, i32, P, P, P, P]
             L.tacg_group_objective.argtypes = [P, i32, i32, P, i32, i32, P, P, P]
             L.tacg_jain.argtypes = [P, i32, i32, i32, i32, P, P, P]
@@ -244,6 +246,25 @@ def eval_online(trace: torch.Tensor, fam_off, n_experts: int, home_start, home_s
     _check("tacg_eval_online", st)
     out["err"] = err
     return out
+
+
+def activation_distance(D: torch.Tensor, top_k: int, stream=None) -> torch.Tensor:
+    """float64 [F][F] Frobenius distances of the families' expert-activation distributions."""
+    F, L_, E = D.shape
+    out = torch.empty((F, F), dtype=torch.float64, device=D.device)
+    st = lib().tacg_activation_distance(_dptr(D), F, L_, E, top_k, _dptr(out), _stream(stream))
+    _check("tacg_activation_distance", st)
+    return out
+
+
+def pair_jaccard(C: torch.Tensor, top_n: int = 64, stream=None):
+    """(top_pairs int32 [F][L][top_n], jaccard float64 [L][F][F]) of the co-activation counts."""
+    F, L_, E, _ = C.shape
+    pairs = torch.empty((F, L_, top_n), dtype=torch.int32, device=C.device)
+    jac = torch.empty((L_, F, F), dtype=torch.float64, device=C.device)
+    st = lib().tacg_pair_jaccard(_dptr(C), F, L_, E, top_n, _dptr(pairs), _dptr(jac), _stream(stream))
+    _check("tacg_pair_jaccard", st)
+    return pairs, jac
 
 
 def gesr_scores(D: torch.Tensor, C: torch.Tensor, top_k: int, stream=None):

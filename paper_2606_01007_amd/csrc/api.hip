@@ -78,6 +78,23 @@ int tacg_gesr_scores(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_
   return tacg::launch_gesr_scores(D, C, n_fam, n_layers, n_experts, top_k, cent, cons, spec, as_stream(hip_stream));
 }
 
+int tacg_activation_distance(const uint32_t* D, int32_t n_fam, int32_t n_layers, int32_t n_experts, int32_t top_k,
+                             double* dist, void* hip_stream) {
+  if (D == nullptr || dist == nullptr) return TACG_E_INVAL;
+  if (n_fam < 1 || n_layers < 1 || n_experts < 1 || top_k < 1 || top_k > n_experts) return TACG_E_INVAL;
+  if (n_experts > TACG_MAX_EXPERTS || n_fam > TACG_MAX_FAMILIES || top_k > TACG_MAX_TOPK) return TACG_E_UNSUPPORTED;
+  return tacg::launch_activation_distance(D, n_fam, n_layers, n_experts, top_k, dist, as_stream(hip_stream));
+}
+
+int tacg_pair_jaccard(const uint32_t* C, int32_t n_fam, int32_t n_layers, int32_t n_experts, int32_t top_n,
+                      int32_t* top_pairs, double* jaccard, void* hip_stream) {
+  if (C == nullptr || top_pairs == nullptr || jaccard == nullptr) return TACG_E_INVAL;
+  if (n_fam < 1 || n_layers < 1 || n_experts < 2 || top_n < 1) return TACG_E_INVAL;
+  if (n_experts > TACG_MAX_EXPERTS || n_fam > TACG_MAX_FAMILIES || top_n > TACG_MAX_TOP_PAIRS || n_layers > 65535)
+    return TACG_E_UNSUPPORTED;
+  return tacg::launch_pair_jaccard(C, n_fam, n_layers, n_experts, top_n, top_pairs, jaccard, as_stream(hip_stream));
+}
+
 int tacg_placement_load(const uint32_t* D, int32_t n_fam, int32_t n_layers, int32_t n_experts,
                         const uint8_t* primary, int32_t n_place, int32_t n_gpus, int64_t* load_ref, uint32_t* d_err,
                         void* hip_stream) {

@@ -42,6 +42,11 @@ int launch_reweight(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t
 int launch_gesr_scores(const uint32_t* D, const uint32_t* C, int32_t n_fam, int32_t n_layers, int32_t n_experts,
                        int32_t top_k, double* cent, double* cons, double* spec, hipStream_t stream);
 
+int launch_activation_distance(const uint32_t* D, int32_t n_fam, int32_t n_layers, int32_t n_experts, int32_t top_k,
+                               double* dist, hipStream_t stream);
+int launch_pair_jaccard(const uint32_t* C, int32_t n_fam, int32_t n_layers, int32_t n_experts, int32_t top_n,
+                        int32_t* top_pairs, double* jaccard, hipStream_t stream);
+
 // ---- placement scoring ---------------------------------------------------------------------
 size_t eval_workspace(int64_t n_tokens, int32_t n_layers, int32_t n_experts, int32_t n_gpus, int32_t n_place,
                       int32_t n_fam);

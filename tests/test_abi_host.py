@@ -154,6 +154,14 @@ def test_eval_online_argument_errors(L):
     assert call(off_=np.array([0, 60, 90], dtype=np.int64)) == tacg.E_INVAL
 
 
+def test_diagnostics_argument_errors(L):
+    assert L.tacg_activation_distance(None, 2, 2, 8, 2, FAKE, None) == tacg.E_INVAL
+    assert L.tacg_activation_distance(FAKE, 2, 2, 300, 2, FAKE, None) == tacg.E_UNSUPPORTED
+    assert L.tacg_pair_jaccard(FAKE, 2, 2, 1, 64, FAKE, FAKE, None) == tacg.E_INVAL
+    assert L.tacg_pair_jaccard(FAKE, 2, 2, 8, 0, FAKE, FAKE, None) == tacg.E_INVAL
+    assert L.tacg_pair_jaccard(FAKE, 2, 2, 8, 5000, FAKE, FAKE, None) == tacg.E_UNSUPPORTED
+
+
 def test_gesr_scores_argument_errors(L):
     assert L.tacg_gesr_scores(FAKE, FAKE, 2, 2, 300, 2, FAKE, FAKE, FAKE, None) == tacg.E_UNSUPPORTED
     assert L.tacg_gesr_scores(FAKE, FAKE, 0, 2, 8, 2, FAKE, FAKE, FAKE, None) == tacg.E_INVAL

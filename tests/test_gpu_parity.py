@@ -458,3 +458,37 @@ def test_gesr_scores_empty_family():
     co, so, po = oracle.gesr_scores(Do, Co, 3)
     np.testing.assert_allclose(cons.cpu().numpy(), so, rtol=1e-12, atol=1e-15)
     np.testing.assert_allclose(spec.cpu().numpy(), po, rtol=1e-12, atol=1e-15)
+
+
+# ------------------------------------------------------------------------------------------------
+# motivation diagnostics
+# ------------------------------------------------------------------------------------------------
+@pytest.mark.parametrize("name", ["tiny", "deepseek16b", "qwen15", "qwen3_30b", "deepseek_v3"])
+def test_diagnostics_parity(name):
+    cfg = synth.CONFIGS[name]
+    _say(f"diagnostics {name}")
+    n = cfg.tokens_group if name == "tiny" else cfg.F * 900 + 7
+    w = synth.make_workload(name, n_tokens=n, layers=min(cfg.L, 3), n_place=2)
+    D, C, err = tacg.coact_build(w.trace_group.cuda(), w.fam_off_group, cfg.E)
+    dist = tacg.activation_distance(D, cfg.k)
+    pairs, jac = tacg.pair_jaccard(C, 64)
+    assert _err(err) == 0
+    Do, Co, _ = oracle.coact(w.trace_group, w.fam_off_group, cfg.E)
+    np.testing.assert_allclose(dist.cpu().numpy(), oracle.activation_distance(Do, cfg.k), rtol=1e-12, atol=1e-15)
+    np.testing.assert_array_equal(pairs.cpu().numpy(), oracle.top_pairs(Co, 64))
+    np.testing.assert_array_equal(jac.cpu().numpy(), oracle.pair_jaccard(Co, 64))
+
+
+@pytest.mark.parametrize("E,top_n,vmax,seed", [(2, 1, 3, 1), (9, 5, 2, 2), (60, 64, 3, 3), (256, 4096, 100000, 4),
+                                              (128, 200, 1, 5), (256, 64, 0, 6)])
+def test_top_pairs_ties_and_edges(E, top_n, vmax, seed):
+    """Dense symmetric counts with many ties (vmax small), all-zero counts and top_n above the number
+    of pairs."""
+    rng = np.random.default_rng(seed)
+    F, L = 3, 2
+    C = rng.integers(0, vmax + 1, size=(F, L, E, E)).astype(np.int64)
+    C = np.triu(C, 1)
+    C = C + C.transpose(0, 1, 3, 2)
+    pairs, jac = tacg.pair_jaccard(torch.as_tensor(C.astype(np.int32)).cuda(), top_n)
+    np.testing.assert_array_equal(pairs.cpu().numpy(), oracle.top_pairs(C, top_n))
+    np.testing.assert_array_equal(jac.cpu().numpy(), oracle.pair_jaccard(C, top_n))
