@@ -31,27 +31,28 @@ CALIB_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 
 
-def source_digest() -> str:
-    """SHA-256 over the HIP sources; HBM traffic figures are only reported for the kernels they
-    were measured on."""
-    import glob
+def source_digest(files) -> str:
+    """SHA-256 over the HIP sources that hold one kernel (and the shared internal header): HBM
+    traffic figures are only reported for the kernel code they were measured on."""
     import hashlib
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2606_01007_amd", "csrc", "*"))):
-        h.update(open(f, "rb").read())
+    for f in sorted(set(files) | {"tacg_internal.h"}):
+        h.update(f.encode())
+        h.update(open(os.path.join(ROOT, "paper_2606_01007_amd", "csrc", f), "rb").read())
     return h.hexdigest()
 
 
 def measured_traffic(kernel: str, workload: str):
-    """Per-launch HBM bytes of `kernel` from profiles/hbm_traffic.json, if measured on these sources."""
+    """Per-launch HBM bytes of `kernel` from profiles/hbm_traffic.json, if measured on its current
+    sources and on this workload."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    if rec.get("source_sha256") != source_digest():
-        return None
     k = rec.get("kernels", {}).get(kernel)
     if not k or k.get("workload") != workload:
+        return None
+    if k.get("source_sha256") != source_digest(TRAFFIC_KERNELS[kernel][1]):
         return None
     return k.get("bytes_per_launch")
 
@@ -80,8 +81,9 @@ def parse():
     return ap.parse_args()
 
 
-# kernels whose HBM bytes are reported, and the device kernels each one is made of
-TRAFFIC_KERNELS = {"ev_main": ("ev_main",), "coact_build": ("coact_hist_kernel", "coact_reduce_kernel")}
+# kernels whose HBM bytes are reported: the device kernels each one is made of, and their sources
+TRAFFIC_KERNELS = {"ev_main": (("ev_main",), ("eval.hip",)),
+                   "coact_build": (("coact_hist_kernel", "coact_reduce_kernel"), ("coact.hip",))}
 
 
 def write_traffic(fetch_csv: str, write_csv: str, workload: str) -> dict:
@@ -91,7 +93,7 @@ def write_traffic(fetch_csv: str, write_csv: str, workload: str) -> dict:
     timed region (the largest copy kernel of the run): bytes = KiB * 1024 * (2^30 / copy bytes)."""
     import csv
     import re
-    out = {"source_sha256": source_digest(), "kernels": {}, "scale": {}}
+    out = {"kernels": {}, "scale": {}}
     per = {}
     for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
         rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
@@ -106,12 +108,12 @@ def write_traffic(fetch_csv: str, write_csv: str, workload: str) -> dict:
             if m:
                 sums.setdefault(m.group(1), []).append(float(r["Counter_Value"]) * 1024.0 * scale)
         per[counter] = {k: sum(v) / len(v) for k, v in sums.items()}
-    for name, parts in TRAFFIC_KERNELS.items():
+    for name, (parts, files) in TRAFFIC_KERNELS.items():
         if all(p in per["FETCH_SIZE"] and p in per["WRITE_SIZE"] for p in parts):
             f = sum(per["FETCH_SIZE"][p] for p in parts)
             w = sum(per["WRITE_SIZE"][p] for p in parts)
             out["kernels"][name] = {"workload": workload, "fetch_bytes": f, "write_bytes": w,
-                                    "bytes_per_launch": f + w}
+                                    "bytes_per_launch": f + w, "source_sha256": source_digest(files)}
     os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
     with open(TRAFFIC_FILE, "w") as fh:
         json.dump(out, fh, indent=1)
