@@ -70,7 +70,7 @@ def _load():
             lib.oracle_coact.argtypes = [P, i64, i32, i32, i32, P, i32, P, P]
             lib.oracle_coact.restype = ctypes.c_int
             lib.oracle_score.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, i32, i32,
-                                         P, P, i32, P, i32, i32, P, P, P, P]
+                                         P, P, i32, P, i32, i32, P, P, P, P, P, P, P]
             lib.oracle_score.restype = ctypes.c_int
             lib.oracle_score_online.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, i32, i32,
                                                 P, P, i32, ctypes.c_double, i32, i32, P, P, P, P, P, P]
@@ -203,9 +203,10 @@ def placement_load(D, primary, n_gpus: int):
 
 
 def score(trace, fam_off, n_experts: int, home_start, home_size, n_gpus: int, primary,
-          secondary=None, load_ref=None, theta=(3, 20), p_range=None):
+          secondary=None, load_ref=None, theta=(3, 20), p_range=None, stats=False):
     """Returns dict(cost_home [P], cost_span [P], load [P][L][G], cost_home_fam [P][F], err) (int64).
-    Only placements in p_range = (p0, p1) are scored (others left zero)."""
+    Only placements in p_range = (p0, p1) are scored (others left zero).  stats=True adds the
+    per-token statistics of App. C per family: span_fam, cross_fam, home_mass_fam ([P][F])."""
     tr = _np(trace, np.int16)
     L, N, k = tr.shape
     off = _np(fam_off, np.int64)
@@ -225,11 +226,15 @@ def score(trace, fam_off, n_experts: int, home_start, home_size, n_gpus: int, pr
     cost_span = np.zeros(P, dtype=np.int64)
     load = np.zeros((P, L, n_gpus), dtype=np.int64)
     fam = np.zeros((P, F), dtype=np.int64)
+    st = [np.zeros((P, F), dtype=np.int64) for _ in range(3)] if stats else [None, None, None]
     tn, td = theta if theta is not None else (0, 0)
     err = _load().oracle_score(_ptr(tr), N, L, k, n_experts, _ptr(off), F, _ptr(hs), _ptr(hz), n_gpus, P, p0, p1,
                                _ptr(prim), _ptr(sec), R, _ptr(ref), int(tn), int(td),
-                               _ptr(cost_home), _ptr(cost_span), _ptr(load), _ptr(fam))
-    return dict(cost_home=cost_home, cost_span=cost_span, load=load, cost_home_fam=fam, err=int(err))
+                               _ptr(cost_home), _ptr(cost_span), _ptr(load), _ptr(fam), *[_ptr(a) for a in st])
+    out = dict(cost_home=cost_home, cost_span=cost_span, load=load, cost_home_fam=fam, err=int(err))
+    if stats:
+        out.update(span_fam=st[0], cross_fam=st[1], home_mass_fam=st[2])
+    return out
 
 
 def score_online(trace, fam_off, n_experts: int, home_start, home_size, n_gpus: int, primary,

@@ -13,7 +13,8 @@
  *   oracle_coact          -- all segments (OpenMP over independent segments).
  *   oracle_score          -- per placement: cross-GPU cost, GESR candidate choice and per-GPU loads
  *                            (Sec. 3.4 eqs. mean-load, feasible-set and the fallback after it; the
- *                            per-token dispatch sets of App. C; the dispatch loads of App. H).
+ *                            per-token dispatch sets of App. C; the dispatch loads of App. H), and
+ *                            optionally the per-token trace statistics of App. C per family.
  *   oracle_score_online   -- the same with the guard and the least-loaded choice reading decayed
  *                            per-GPU loads updated after every token (Sec. 3.4 eq. load-update).
  *
@@ -134,6 +135,12 @@ static void feasible_gpus(const int64_t* ref, int32_t G, int32_t theta_num, int3
  *   cost_span[p]      += |cards| - 1          (the per-layer cross-group dispatch count of App. C)
  *   load[p][l][m]     += number of the token's experts served by m
  *   cost_home_fam[p][f] += |cards \ {h}|      (may be NULL)
+ * and, when span_fam / cross_fam / home_mass_fam are not NULL, the per-token trace statistics of
+ * App. C per family f of the token:
+ *   span_fam[p][f]      += |cards| - 1        (cross-group dispatch count)
+ *   cross_fam[p][f]     += 1 when no family band [home_start, home_start + home_size) contains
+ *                          every card (the layer spans more than one family)
+ *   home_mass_fam[p][f] += number of slots served by a GPU in f's own band (home-family mass)
  * Tables: primary [P][L][E], secondary [P][L][E][R] (0xFF = none, may be NULL when R = 0),
  * load_ref [P][L][G] (required when R > 0).  Outputs of the placements scored are overwritten.
  */
@@ -142,9 +149,11 @@ int oracle_score(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32
                  int32_t n_gpus, int32_t n_place, int32_t p_begin, int32_t p_end,
                  const uint8_t* primary, const uint8_t* secondary, int32_t n_sec,
                  const int64_t* load_ref, int32_t theta_num, int32_t theta_den,
-                 int64_t* cost_home, int64_t* cost_span, int64_t* load, int64_t* cost_home_fam)
+                 int64_t* cost_home, int64_t* cost_span, int64_t* load, int64_t* cost_home_fam,
+                 int64_t* span_fam, int64_t* cross_fam, int64_t* home_mass_fam)
 {
     const int32_t E = n_experts, k = top_k, G = n_gpus, L = n_layers, R = n_sec;
+    const int stats = span_fam != NULL && cross_fam != NULL && home_mass_fam != NULL;
     int err = 0;
     if (G < 1 || G > 32 || k < 1 || k > 16 || k > E || E > 256 || R < 0 || R > 4 || n_fam < 1 || n_fam > 64 ||
         p_begin < 0 || p_end > n_place || p_begin > p_end) return ORC_ERR_ARG;
@@ -159,6 +168,12 @@ int oracle_score(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32
         cost_span[p] = 0;
         if (cost_home_fam)
             for (int32_t f = 0; f < n_fam; ++f) cost_home_fam[(int64_t)p * n_fam + f] = 0;
+        if (stats)
+            for (int32_t f = 0; f < n_fam; ++f) {
+                span_fam[(int64_t)p * n_fam + f] = 0;
+                cross_fam[(int64_t)p * n_fam + f] = 0;
+                home_mass_fam[(int64_t)p * n_fam + f] = 0;
+            }
     }
     const int64_t n_pl = (int64_t)(p_end - p_begin) * L;
 #pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
@@ -171,6 +186,8 @@ int oracle_score(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32
         for (int32_t m = 0; m < G; ++m) ld[m] = 0;
         int feas[32];
         feasible_gpus(ref, G, theta_num, theta_den, feas);
+        int64_t st_span[64], st_cross[64], st_mass[64];
+        for (int32_t f = 0; f < n_fam && f < 64; ++f) st_span[f] = st_cross[f] = st_mass[f] = 0;
 
         /* candidate set C_{l,e} of eq. candidate-set, and its feasible part (fallback: all) */
         int n_cand[256], cand[256][5], fc[256][32];
@@ -233,6 +250,19 @@ int oracle_score(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32
                 span_acc += n_cards - 1;
                 if (f < 64) fam_acc[f] += home_cost;
                 for (int32_t s = 0; s < k; ++s) ld[slot_gpu[s]] += 1;
+                if (stats && f < 64) {
+                    st_span[f] += n_cards - 1;
+                    int within_one = 0;
+                    for (int32_t f2 = 0; f2 < n_fam && !within_one; ++f2) {
+                        int inside = 1;
+                        for (int32_t m = 0; m < G; ++m)
+                            if (in_r[m] && (m < home_start[f2] || m >= home_start[f2] + home_size[f2])) inside = 0;
+                        within_one = inside;
+                    }
+                    st_cross[f] += !within_one;
+                    for (int32_t s = 0; s < k; ++s)
+                        st_mass[f] += slot_gpu[s] >= home_start[f] && slot_gpu[s] < home_start[f] + home_size[f];
+                }
             }
         }
 #pragma omp atomic
@@ -243,6 +273,15 @@ int oracle_score(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32
             for (int32_t f = 0; f < n_fam && f < 64; ++f) {
 #pragma omp atomic
                 cost_home_fam[(int64_t)p * n_fam + f] += fam_acc[f];
+            }
+        if (stats)
+            for (int32_t f = 0; f < n_fam && f < 64; ++f) {
+#pragma omp atomic
+                span_fam[(int64_t)p * n_fam + f] += st_span[f];
+#pragma omp atomic
+                cross_fam[(int64_t)p * n_fam + f] += st_cross[f];
+#pragma omp atomic
+                home_mass_fam[(int64_t)p * n_fam + f] += st_mass[f];
             }
     }
     return err;

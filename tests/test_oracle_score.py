@@ -247,3 +247,117 @@ def test_table_errors_flagged(oracle_mod):
     prim[1, 0, 3] = 4
     r = oracle_mod.score(w.trace_serve, w.fam_off_serve, 8, ps["home_start"], ps["home_size"], 4, prim)
     assert r["err"] & oracle_mod.ERR_TABLE
+
+
+# ---------------------------------------------------------------------------------------------
+# per-token trace statistics of App. C (cross-group dispatches, cross-family layers, home-family
+# dispatch mass) per family
+# ---------------------------------------------------------------------------------------------
+def brute_stats(tr, off, E, hs, hz, G, prim, sec=None, ref=None, theta=(3, 20)):
+    """Independent pure-Python statistics: resolve every slot as in brute_score, then apply the
+    three definitions with Python sets."""
+    L, N, k = tr.shape
+    P = prim.shape[0]
+    F = len(off) - 1
+    span = np.zeros((P, F), dtype=np.int64)
+    cross = np.zeros((P, F), dtype=np.int64)
+    mass = np.zeros((P, F), dtype=np.int64)
+    bands = [set(range(int(hs[f]), int(hs[f]) + int(hz[f]))) for f in range(F)]
+    for p in range(P):
+        for l in range(L):
+            if ref is not None and theta[1] > 0:
+                bound = (1 + Fraction(theta[0], theta[1])) * Fraction(int(ref[p, l].sum()), G)
+                feas = {m for m in range(G) if ref[p, l, m] <= bound}
+            else:
+                feas = set(range(G))
+            cands = {e: [int(prim[p, l, e])] + ([int(g) for g in sec[p, l, e] if g != NONE] if sec is not None
+                                                 else []) for e in range(E)}
+            for f in range(F):
+                for t in range(off[f], off[f + 1]):
+                    h = int(hs[f] + (t - off[f]) % hz[f])
+                    ids = [int(x) for x in tr[l, t]]
+                    gpu = {s: cands[e][0] for s, e in enumerate(ids) if len(cands[e]) == 1}
+                    R = set(gpu.values())
+                    for s, e in enumerate(ids):
+                        if s in gpu:
+                            continue
+                        FC = set(cands[e]) & feas or set(cands[e])
+                        pick = min(FC & R) if FC & R else (h if h in FC else
+                                                            min(FC, key=lambda m: (int(ref[p, l, m]), m)))
+                        gpu[s] = pick
+                        R.add(pick)
+                    span[p, f] += len(R) - 1
+                    cross[p, f] += not any(R <= b for b in bands)
+                    mass[p, f] += sum(gpu[s] in bands[f] for s in range(k))
+    return span, cross, mass
+
+
+def _check_stats(oracle_mod, tr, off, E, hs, hz, G, prim, sec=None, ref=None, theta=(3, 20)):
+    r = oracle_mod.score(tr, off, E, hs, hz, G, prim, sec, ref, theta, stats=True)
+    assert r["err"] == 0
+    span, cross, mass = brute_stats(np.asarray(tr), off, E, hs, hz, G, prim, sec, ref, theta)
+    np.testing.assert_array_equal(r["span_fam"], span)
+    np.testing.assert_array_equal(r["cross_fam"], cross)
+    np.testing.assert_array_equal(r["home_mass_fam"], mass)
+    np.testing.assert_array_equal(r["span_fam"].sum(axis=1), r["cost_span"])
+    return r
+
+
+def test_trace_stats_hand_worked(oracle_mod):
+    """G = 4 in two bands {0, 1} and {2, 3}; expert e on GPU e; k = 2, one layer.
+    family 0: {0,1} (inside band 0, 2 home slots), {0,2} (spans both, 1 home slot);
+    family 1: {2,3} (inside, 2), {1,3} (spans, 1), {3,2} (inside, 2)."""
+    tr = np.array([[[0, 1], [0, 2], [2, 3], [1, 3], [3, 2]]], dtype=np.int16)
+    prim = np.arange(4, dtype=np.uint8)[None, None]
+    r = oracle_mod.score(tr, [0, 2, 5], 4, [0, 2], [2, 2], 4, prim, stats=True)
+    assert r["err"] == 0
+    np.testing.assert_array_equal(r["span_fam"], [[2, 3]])
+    np.testing.assert_array_equal(r["cross_fam"], [[1, 1]])
+    np.testing.assert_array_equal(r["home_mass_fam"], [[3, 5]])
+
+
+@pytest.mark.parametrize("name,setidx", [("tiny", 0), ("qwen15", 0), ("qwen15", 1), ("deepseek_v3", 0)])
+def test_trace_stats_brute(oracle_mod, name, setidx):
+    cfg = synth.CONFIGS[name]
+    w = synth.make_workload(name, n_tokens=cfg.F * 19, layers=2, n_place=3)
+    ps = w.placement_sets[setidx]
+    G = ps["n_gpus"]
+    ref = None
+    if ps["secondary"] is not None:
+        D, _, _ = oracle_mod.coact(w.trace_serve, w.fam_off_serve, cfg.E)
+        ref = oracle_mod.placement_load(D, ps["primary"], G)
+    _check_stats(oracle_mod, w.trace_serve.numpy(), w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], G,
+                 ps["primary"], ps["secondary"], ref)
+
+
+def test_trace_stats_mass_from_counts(oracle_mod):
+    """Without replicas every slot of expert e goes to its primary, so the home-family mass is the
+    family's dispatch count of the experts placed in its band: sum_l sum_{e: prim(e) in band f} D_f[l][e]
+    (D from the independent counting pass)."""
+    w = synth.make_workload("qwen3_30b", n_tokens=16 * 40, layers=3, n_place=4)
+    ps = w.placement_sets[0]
+    G = ps["n_gpus"]
+    D, _, _ = oracle_mod.coact(w.trace_serve, w.fam_off_serve, 128)
+    r = oracle_mod.score(w.trace_serve, w.fam_off_serve, 128, ps["home_start"], ps["home_size"], G, ps["primary"],
+                         stats=True)
+    hs, hz = ps["home_start"], ps["home_size"]
+    for p in range(ps["primary"].shape[0]):
+        inb = [(ps["primary"][p] >= hs[f]) & (ps["primary"][p] < hs[f] + hz[f]) for f in range(len(hs))]
+        expect = [int((D[f] * inb[f]).sum()) for f in range(len(hs))]
+        np.testing.assert_array_equal(r["home_mass_fam"][p], expect)
+
+
+def test_trace_stats_degenerate_bands(oracle_mod):
+    """One band holding every GPU: no layer spans two families and every slot is home mass.
+    One GPU per band (G = F): a layer is cross-family exactly when it touches two or more GPUs."""
+    w = synth.make_workload("deepseek16b", n_tokens=8 * 50, layers=2, n_place=3)
+    ps = w.placement_sets[0]
+    N, L, k, G, F = 8 * 50, 2, 6, 8, 8
+    r = oracle_mod.score(w.trace_serve, w.fam_off_serve, 64, [0] * F, [G] * F, G, ps["primary"], stats=True)
+    assert np.all(r["cross_fam"] == 0)
+    np.testing.assert_array_equal(r["home_mass_fam"].sum(axis=1), [N * L * k] * 3)
+    r = oracle_mod.score(w.trace_serve, w.fam_off_serve, 64, np.arange(F), [1] * F, G, ps["primary"], stats=True)
+    tr = w.trace_serve.numpy()
+    for p in range(3):
+        n_multi = sum(len({int(ps["primary"][p, l, e]) for e in tr[l, t]}) >= 2 for l in range(L) for t in range(N))
+        assert int(r["cross_fam"][p].sum()) == n_multi
