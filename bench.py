@@ -340,7 +340,8 @@ def placement_quality(w, ps, cfg, D, C, err):
     """Untimed context: the paper's communication metric (App. H "Comm": mean over tokens of
     sum_l (|cards_l| - 1)) on the serving trace, for the contiguous default placement and for the
     TACG placement grouped on the host from this run's A-tilde (grouping trace) with GESR replicas
-    (generic experts by centrality, secondaries by affinity), plus Jain and MaxVio."""
+    (generic experts by centrality, secondaries by affinity), plus Jain and MaxVio and the per-token
+    statistics of App. C (layers spanning more than one family band, home-family dispatch mass)."""
     import numpy as np
     import torch
 
@@ -368,19 +369,27 @@ def placement_quality(w, ps, cfg, D, C, err):
     if sec_t is not None:
         Ds, _, _ = tacg.coact_build(w.trace_serve, w.fam_off_serve, E, err=err)
         ref = tacg.placement_load(Ds, prim_t, G, err=err)
-    out = tacg.eval_placements(w.trace_serve, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, prim_t,
-                               sec_t, ref, theta=(3, 20), err=err)
+    out = tacg.eval_trace_stats(w.trace_serve, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, prim_t,
+                                sec_t, ref, theta=(3, 20), err=err)
     jn, mv = tacg.jain_index(out["load"])
     torch.cuda.synchronize()
     Ns = w.trace_serve.shape[1]
     span = out["cost_span"].cpu().numpy().astype(np.float64) / Ns
     home = out["cost_home"].cpu().numpy().astype(np.float64) / Ns
+    # App. C per-token statistics, averaged over the families that have tokens
+    nf = np.diff(np.asarray(w.fam_off_serve, dtype=np.int64)).astype(np.float64)
+    has = nf > 0
+    cross = out["cross_fam"].cpu().numpy()[:, has] / nf[has]
+    mass = out["home_mass_fam"].cpu().numpy()[:, has] / (nf[has] * L * k)
     return {"placements": "contiguous default vs TACG (host spectral grouping of this run's A-tilde, alpha=0.25)"
                           f" with GESR ({n_rep} generic experts by centrality x {n_sec} secondaries by affinity)",
             "trace": "serving trace (synthetic)",
             "comm_default": span[0], "comm_tacg": span[1],
             "comm_reduction_pct": 100.0 * (span[0] - span[1]) / span[0] if span[0] > 0 else None,
             "home_cost_default": home[0], "home_cost_tacg": home[1],
+            "cross_family_layers_per_token": [float(cross[0].mean()), float(cross[1].mean())],
+            "home_family_mass_pct": [float(100 * mass[0].mean()), float(100 * mass[1].mean())],
+            "home_family_mass_uniform_pct": float(100 * np.mean(np.asarray(ps["home_size"])[has] / G)),
             "jain": [float(jn[0]), float(jn[1])], "maxvio": [float(mv[0]), float(mv[1])],
             "host_s": time.time() - t0}
 

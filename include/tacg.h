@@ -176,6 +176,30 @@ size_t tacg_eval_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t n_e
                                  int32_t n_place, int32_t n_fam);
 
 /*
+ * The per-token trace statistics of App. C, per placement and family f, on top of everything
+ * tacg_eval_placements computes (same arguments, same choice rule, same outputs):
+ *   span_fam[p][f]      = sum over f's tokens t and layers l of |cards_l(t)| - 1
+ *                         (cross-group dispatches; sum over f equals cost_span[p])
+ *   cross_fam[p][f]     = number of (t, l) whose card set is not contained in one family band
+ *                         (layers that span more than one family)
+ *   home_mass_fam[p][f] = number of (t, l, slot) whose serving GPU lies in f's own band
+ *                         [home_start[f], home_start[f] + home_size[f]) (home-family dispatch mass;
+ *                         divide by N_f * L * k for the share)
+ * All three uint64 [P][F], device memory.  Family bands are the caller's home bands; the distinct
+ * bands must tile 0..G-1 without overlap (as the default bands do for every F and G), else
+ * TACG_E_UNSUPPORTED.  Costs about 8 more integer ops per placement-token-layer than
+ * tacg_eval_placements.  Workspace: tacg_eval_workspace_bytes(...) bytes.  flags: must be 0.
+ */
+int tacg_eval_trace_stats(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
+                          int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam,
+                          const int32_t* home_start_host, const int32_t* home_size_host, int32_t n_gpus,
+                          int32_t n_place, const uint8_t* primary, const uint8_t* secondary_or_null,
+                          int32_t n_sec, const int64_t* load_ref_or_null, int32_t theta_num,
+                          int32_t theta_den, uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
+                          uint64_t* span_fam, uint64_t* cross_fam, uint64_t* home_mass_fam, uint32_t flags,
+                          uint32_t* d_err, void* workspace, size_t workspace_bytes, void* hip_stream);
+
+/*
  * Placement scoring with decayed per-GPU loads: the sequential form of the serving rule of Sec. 3.4
  * (eqs. mean-load, feasible-set and load-update).  Same choice rule, costs and loads as
  * tacg_eval_placements, but every (placement p, layer l) keeps its own loads L_m, which the guard and

@@ -62,6 +62,8 @@ def lib():
             L.tacg_placement_load.argtypes = [P, i32, i32, i32, P, i32, i32, P, P, P]
             L.tacg_eval_placements.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, P, P, i32, P, i32, i32,
                                                P, P, P, P, u32, P, P, sz, P]
+            L.tacg_eval_trace_stats.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, P, P, i32, P, i32,
+                                                i32, P, P, P, P, P, P, u32, P, P, sz, P]
             L.tacg_eval_workspace_bytes.argtypes = [i64, i32, i32, i32, i32, i32]
             L.tacg_eval_workspace_bytes.restype = sz
             L.tacg_eval_online.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, P, P, i32, f64, i32, i32,
@@ -74,7 +76,7 @@ def lib():
             L.tacg_strerror.argtypes = [ctypes.c_int]
             L.tacg_strerror.restype = ctypes.c_char_p
             for name in ("tacg_coact_build", "tacg_reweight", "tacg_placement_load", "tacg_eval_placements",
-                         "tacg_jain"):
+                         "tacg_eval_trace_stats", "tacg_jain"):
                 getattr(L, name).restype = ctypes.c_int
             _lib = L
     return _lib
@@ -210,6 +212,41 @@ def eval_placements(trace: torch.Tensor, fam_off, n_experts: int, home_start, ho
         _dptr(out["cost_home"]), _dptr(out["cost_span"]), _dptr(out["load"]), _dptr(out["cost_home_fam"]), 0,
         _dptr(err), _dptr(ws), ws.numel(), _stream(stream))
     _check("tacg_eval_placements", st)
+    out["err"] = err
+    return out
+
+
+def eval_trace_stats(trace: torch.Tensor, fam_off, n_experts: int, home_start, home_size, n_gpus: int,
+                     primary: torch.Tensor, secondary: Optional[torch.Tensor] = None,
+                     load_ref: Optional[torch.Tensor] = None, theta=(3, 20), ws: Optional[torch.Tensor] = None,
+                     err: Optional[torch.Tensor] = None, stream=None) -> dict:
+    """Snapshot scoring plus the per-token statistics of App. C (tacg_eval_trace_stats).
+    dict(cost_home, cost_span, load, span_fam, cross_fam, home_mass_fam ([P][F] int64), err)."""
+    L_, N, k = trace.shape
+    off = _host_i64(fam_off)
+    F = off.size - 1
+    hs, hz = _host_i32(home_start), _host_i32(home_size)
+    P = primary.shape[0]
+    dev = trace.device
+    R = 0 if secondary is None else int(secondary.shape[-1])
+    out = dict(cost_home=torch.empty(P, dtype=torch.int64, device=dev),
+               cost_span=torch.empty(P, dtype=torch.int64, device=dev),
+               load=torch.empty((P, L_, n_gpus), dtype=torch.int32, device=dev),
+               span_fam=torch.empty((P, F), dtype=torch.int64, device=dev),
+               cross_fam=torch.empty((P, F), dtype=torch.int64, device=dev),
+               home_mass_fam=torch.empty((P, F), dtype=torch.int64, device=dev))
+    need = lib().tacg_eval_workspace_bytes(N, L_, n_experts, n_gpus, P, F)
+    if ws is None or ws.numel() < need:
+        ws = workspace(need, dev)
+    if err is None:
+        err = _err_tensor(dev)
+    tn, td = theta if theta is not None else (0, 0)
+    st = lib().tacg_eval_trace_stats(
+        _dptr(trace), N, L_, k, n_experts, _hptr(off), F, _hptr(hs), _hptr(hz), n_gpus, P, _dptr(primary),
+        _dptr(secondary) if R > 0 else None, R, _dptr(load_ref) if R > 0 else None, int(tn), int(td),
+        _dptr(out["cost_home"]), _dptr(out["cost_span"]), _dptr(out["load"]), _dptr(out["span_fam"]),
+        _dptr(out["cross_fam"]), _dptr(out["home_mass_fam"]), 0, _dptr(err), _dptr(ws), ws.numel(), _stream(stream))
+    _check("tacg_eval_trace_stats", st)
     out["err"] = err
     return out
 

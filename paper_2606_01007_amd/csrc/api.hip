@@ -112,14 +112,17 @@ size_t tacg_eval_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t n_e
   return tacg::eval_workspace(n_tokens, n_layers, n_experts, n_gpus, n_place, n_fam);
 }
 
-int tacg_eval_placements(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
-                         int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam,
-                         const int32_t* home_start_host, const int32_t* home_size_host, int32_t n_gpus,
-                         int32_t n_place, const uint8_t* primary, const uint8_t* secondary_or_null, int32_t n_sec,
-                         const int64_t* load_ref_or_null, int32_t theta_num, int32_t theta_den,
-                         uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
-                         uint64_t* cost_home_fam_or_null, uint32_t flags, uint32_t* d_err, void* workspace,
-                         size_t workspace_bytes, void* hip_stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks shared by the two snapshot-scoring entry points.
+int check_eval(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+               const int64_t* fam_off_host, int32_t n_fam, const int32_t* home_start_host,
+               const int32_t* home_size_host, int32_t n_gpus, int32_t n_place, const uint8_t* primary,
+               const uint8_t* secondary_or_null, int32_t n_sec, const int64_t* load_ref_or_null, int32_t theta_num,
+               int32_t theta_den, const uint64_t* cost_home, const uint64_t* cost_span, const uint32_t* load,
+               uint32_t flags, const uint32_t* d_err, const void* workspace, size_t workspace_bytes) {
   int rc = check_trace(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam);
   if (rc != TACG_OK) return rc;
   if (flags != 0) return TACG_E_INVAL;
@@ -137,9 +140,75 @@ int tacg_eval_placements(const int16_t* trace, int64_t n_tokens, int32_t n_layer
   }
   const size_t need = tacg_eval_workspace_bytes(n_tokens, n_layers, n_experts, n_gpus, n_place, n_fam);
   if (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 256)) return TACG_E_INVAL;
+  return TACG_OK;
+}
+
+// Do the distinct family bands tile 0..G-1 without overlap?  Then every GPU belongs to exactly one
+// band and `starts` gets bit b for every band start b.
+bool bands_tile(const int32_t* home_start, const int32_t* home_size, int32_t n_fam, int32_t G, uint32_t* starts) {
+  int32_t owner_start[TACG_MAX_GPUS], owner_size[TACG_MAX_GPUS];
+  for (int g = 0; g < G; ++g) owner_start[g] = -1;
+  for (int f = 0; f < n_fam; ++f) {
+    for (int g = home_start[f]; g < home_start[f] + home_size[f]; ++g) {
+      if (owner_start[g] < 0) {
+        owner_start[g] = home_start[f];
+        owner_size[g] = home_size[f];
+      } else if (owner_start[g] != home_start[f] || owner_size[g] != home_size[f]) {
+        return false;  // two different bands overlap
+      }
+    }
+  }
+  uint32_t b = 0;
+  for (int g = 0; g < G; ++g) {
+    if (owner_start[g] < 0) return false;  // a GPU outside every band
+    if (owner_start[g] == g) b |= 1u << g;
+  }
+  *starts = b;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+int tacg_eval_placements(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
+                         int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam,
+                         const int32_t* home_start_host, const int32_t* home_size_host, int32_t n_gpus,
+                         int32_t n_place, const uint8_t* primary, const uint8_t* secondary_or_null, int32_t n_sec,
+                         const int64_t* load_ref_or_null, int32_t theta_num, int32_t theta_den,
+                         uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
+                         uint64_t* cost_home_fam_or_null, uint32_t flags, uint32_t* d_err, void* workspace,
+                         size_t workspace_bytes, void* hip_stream) {
+  const int rc = check_eval(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, home_start_host,
+                            home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec, load_ref_or_null,
+                            theta_num, theta_den, cost_home, cost_span, load, flags, d_err, workspace,
+                            workspace_bytes);
+  if (rc != TACG_OK) return rc;
   return tacg::launch_eval(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, home_start_host,
                            home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec, load_ref_or_null,
-                           theta_num, theta_den, cost_home, cost_span, load, cost_home_fam_or_null, d_err, workspace,
+                           theta_num, theta_den, cost_home, cost_span, load, cost_home_fam_or_null, nullptr, d_err,
+                           workspace, as_stream(hip_stream));
+}
+
+int tacg_eval_trace_stats(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
+                          int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam,
+                          const int32_t* home_start_host, const int32_t* home_size_host, int32_t n_gpus,
+                          int32_t n_place, const uint8_t* primary, const uint8_t* secondary_or_null,
+                          int32_t n_sec, const int64_t* load_ref_or_null, int32_t theta_num,
+                          int32_t theta_den, uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
+                          uint64_t* span_fam, uint64_t* cross_fam, uint64_t* home_mass_fam, uint32_t flags,
+                          uint32_t* d_err, void* workspace, size_t workspace_bytes, void* hip_stream) {
+  const int rc = check_eval(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, home_start_host,
+                            home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec, load_ref_or_null,
+                            theta_num, theta_den, cost_home, cost_span, load, flags, d_err, workspace,
+                            workspace_bytes);
+  if (rc != TACG_OK) return rc;
+  if (span_fam == nullptr || cross_fam == nullptr || home_mass_fam == nullptr) return TACG_E_INVAL;
+  tacg::TraceStatsOut st{span_fam, cross_fam, home_mass_fam, 0u};
+  if (!bands_tile(home_start_host, home_size_host, n_fam, n_gpus, &st.band_starts)) return TACG_E_UNSUPPORTED;
+  return tacg::launch_eval(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, home_start_host,
+                           home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec, load_ref_or_null,
+                           theta_num, theta_den, cost_home, cost_span, load, nullptr, &st, d_err, workspace,
                            as_stream(hip_stream));
 }
 

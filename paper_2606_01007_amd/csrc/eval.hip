@@ -45,6 +45,11 @@ struct EvWs {
   unsigned long long* acc_span;  // [P]
   unsigned long long* acc_fam;   // [P][F]
   uint32_t* rep_load;   // [P][L][G]
+  // App. C statistics (used only by tacg_eval_trace_stats)
+  uint32_t* cnt_fam;                  // [F][L][E] dispatches per expert and family
+  unsigned long long* acc_span_fam;   // [P][F] sum of |cards| over the family's token-layers
+  unsigned long long* acc_cross_fam;  // [P][F] token-layers whose cards span several bands
+  unsigned long long* acc_hmass_fam;  // [P][F] replicated-slot dispatches served in the family's band
 };
 
 EvWs carve_ev(void* ws, int32_t L, int32_t E, int32_t G, int32_t P, int32_t F, size_t* used = nullptr) {
@@ -60,6 +65,10 @@ EvWs carve_ev(void* ws, int32_t L, int32_t E, int32_t G, int32_t P, int32_t F, s
   r.rep_list = c.take<int32_t>(static_cast<size_t>(L) * TACG_MAX_REPLICATED);
   r.n_rep = c.take<int32_t>(static_cast<size_t>(L));
   r.rep_info = c.take<uint2>(static_cast<size_t>(L) * TACG_MAX_REPLICATED * P);
+  r.cnt_fam = c.take<uint32_t>(static_cast<size_t>(F) * L * E);
+  r.acc_span_fam = c.take<unsigned long long>(static_cast<size_t>(P) * F);
+  r.acc_cross_fam = c.take<unsigned long long>(static_cast<size_t>(P) * F);
+  r.acc_hmass_fam = c.take<unsigned long long>(static_cast<size_t>(P) * F);
   if (used) *used = c.used;
   return r;
 }
@@ -76,6 +85,10 @@ struct EvArgs {
   int32_t theta_num, theta_den;
   int32_t n_pieces;
   int32_t n_pblocks;  // placement blocks of 64 * PPL placements
+  int32_t stats;      // App. C statistics requested
+  uint32_t band_starts;  // bit b: a family band starts at GPU b (the bands tile 0..G-1)
+  // home band of family f: component f % 4 of band4[f / 4] = home_start | home_size << 8
+  uint4 band4[TACG_MAX_FAMILIES / 4];
   // One record per piece of one family's tokens: (first token, end token, family offset,
   // home_start | home_size << 8 | family << 16).  Kept as 16-byte records: indexing kernel-argument
   // arrays of different element sizes with one runtime index lets the compiler fold the byte and
@@ -97,6 +110,14 @@ __global__ __launch_bounds__(256) void ev_zero(EvArgs a) {
   }
   for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.F; j += stride) w.acc_fam[j] = 0;
   for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.L * a.G; j += stride) w.rep_load[j] = 0;
+  if (a.stats) {
+    for (int64_t j = i; j < static_cast<int64_t>(a.F) * a.L * a.E; j += stride) w.cnt_fam[j] = 0;
+    for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.F; j += stride) {
+      w.acc_span_fam[j] = 0;
+      w.acc_cross_fam[j] = 0;
+      w.acc_hmass_fam[j] = 0;
+    }
+  }
 }
 
 // Table validation and the replicated-expert marks.  Flat grid-stride loop over (p, l, e).
@@ -230,7 +251,7 @@ __device__ __forceinline__ uint32_t find_first_bit(uint32_t x) {
   return r;
 }
 
-template <int K, int PPL, bool NARROW>
+template <int K, int PPL, bool NARROW, bool STATS>
 struct Scorer {
   static constexpr int PW = 64 * PPL;
   static constexpr int KB = (K + 3) / 4;  // dwords of 8-bit expert ids per token-layer
@@ -314,6 +335,8 @@ struct Scorer {
   }
 
   uint32_t home_start;
+  uint32_t band_starts;     // STATS: bit b set when a family band starts at GPU b
+  uint32_t acc_cross[PPL];  // STATS: token-layers whose cards span more than one band
 
   __device__ __forceinline__ void account(uint32_t info, const uint32_t (&m)[PPL]) {
     const uint32_t not_h = ~(1u << (home_start + ((info >> IL::kHomeShift) & 31u)));
@@ -321,19 +344,30 @@ struct Scorer {
     for (int q = 0; q < PPL; ++q) {
       acc_span[q] += __popc(m[q]);
       acc_home[q] += __popc(m[q] & not_h);
+      if constexpr (STATS) {
+        // The bands are intervals that tile the GPUs, so the cards lie in more than one band exactly
+        // when a band starts in (lowest card, highest card].  With lo / hi the lowest / highest card,
+        // (2 << hi) - (2 << lo) (mod 2^32, so hi = 31 works) has exactly those bits set.
+        // (m == 0 only after a flagged table error; the masks keep every shift defined)
+        const uint32_t lo = find_first_bit(m[q]) & 31u;
+        const uint32_t top = 0x80000000u >> (__clz(static_cast<int>(m[q])) & 31);  // 1 << hi
+        const uint32_t range = (top << 1) + (0xfffffffeu << lo);
+        acc_cross[q] += (band_starts & range) != 0u ? 1u : 0u;
+      }
     }
   }
 };
 
 // Token loop of one workgroup (see ev_main).  NARROW: the family's band has at most 4 GPUs, so the
 // fallback choices are packed per band position.
-template <int K, int PPL, bool NARROW>
+template <int K, int PPL, bool NARROW, bool STATS>
 __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl, const uint2* rinfo, uint32_t* rcnt,
                                             uint32_t* ecnt, const uint8_t* rep_of, int l, int p0, int nrep,
                                             bool counter, uint32_t t_begin, uint32_t t_end, uint32_t off_f,
-                                            uint32_t hs, uint32_t hz, uint32_t& err, uint32_t (&acc_span)[PPL],
-                                            uint32_t (&acc_home)[PPL]) {
-  using S = Scorer<K, PPL, NARROW>;
+                                            uint32_t hs, uint32_t hz, int f, uint32_t& err,
+                                            uint32_t (&acc_span)[PPL], uint32_t (&acc_home)[PPL],
+                                            uint32_t (&acc_cross)[PPL], uint32_t& n_scored) {
+  using S = Scorer<K, PPL, NARROW, STATS>;
   using IL = InfoLayout<K>;
   constexpr int PW = S::PW;
   constexpr int KB = S::KB;
@@ -356,8 +390,9 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
   sc.rep_of = rep_of;
   sc.lane = lane;
   sc.home_start = hs;
+  sc.band_starts = a.band_starts;
 #pragma unroll
-  for (int q = 0; q < PPL; ++q) sc.acc_span[q] = sc.acc_home[q] = 0;
+  for (int q = 0; q < PPL; ++q) sc.acc_span[q] = sc.acc_home[q] = sc.acc_cross[q] = 0;
 
   for (uint32_t r_begin = t_begin; r_begin < t_end; r_begin += round_tokens) {
     const uint32_t r_end = min(t_end, r_begin + round_tokens);
@@ -404,6 +439,7 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
         }
       }
       const uint32_t ntile = min(64u, r_end - tile);
+      n_scored += ntile;
       uint32_t j = 0;
       for (; j + U <= ntile; j += U) {
         uint32_t ids[U][KB], tinfo[U];
@@ -457,6 +493,14 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
         uint32_t* dst = a.ws.rep_load + (static_cast<int64_t>(p) * L + l) * G + g;
         if (p < a.P && rsum[2 * c]) atomicAdd(dst, rsum[2 * c]);
         if (p + 1 < a.P && rsum[2 * c + 1]) atomicAdd(dst + static_cast<int64_t>(L) * G, rsum[2 * c + 1]);
+        if constexpr (STATS) {  // replicated-slot dispatches served inside the family's own band
+          if (static_cast<uint32_t>(g) - hs < hz) {
+            unsigned long long* hm = a.ws.acc_hmass_fam + static_cast<int64_t>(p) * a.F + f;
+            if (p < a.P && rsum[2 * c]) atomicAdd(hm, static_cast<unsigned long long>(rsum[2 * c]));
+            if (p + 1 < a.P && rsum[2 * c + 1])
+              atomicAdd(hm + a.F, static_cast<unsigned long long>(rsum[2 * c + 1]));
+          }
+        }
       }
     }
   }
@@ -465,10 +509,11 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
   for (int q = 0; q < PPL; ++q) {
     acc_span[q] = sc.acc_span[q];
     acc_home[q] = sc.acc_home[q];
+    acc_cross[q] = sc.acc_cross[q];
   }
 }
 
-template <int K, int PPL>
+template <int K, int PPL, bool STATS>
 __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
   extern __shared__ __align__(16) uint32_t lds[];
   constexpr int PW = 64 * PPL;
@@ -540,13 +585,14 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
   const int lane = threadIdx.x & 63;
   uint32_t err = 0;
 
-  uint32_t acc_span[PPL], acc_home[PPL];
+  uint32_t acc_span[PPL], acc_home[PPL], acc_cross[PPL];
+  uint32_t n_scored = 0;  // token-layers scored by this wave
   if (hz <= 4) {
-    score_piece<K, PPL, true>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end, off_f, hs, hz,
-                              err, acc_span, acc_home);
+    score_piece<K, PPL, true, STATS>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end, off_f,
+                                     hs, hz, f, err, acc_span, acc_home, acc_cross, n_scored);
   } else {
-    score_piece<K, PPL, false>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end, off_f, hs, hz,
-                               err, acc_span, acc_home);
+    score_piece<K, PPL, false, STATS>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end, off_f,
+                                      hs, hz, f, err, acc_span, acc_home, acc_cross, n_scored);
   }
 
   // ---- flush ----
@@ -559,13 +605,24 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
         atomicAdd(&a.ws.acc_home[p], static_cast<unsigned long long>(acc_home[q]));
         atomicAdd(&a.ws.acc_fam[static_cast<int64_t>(p) * a.F + f], static_cast<unsigned long long>(acc_home[q]));
       }
+      if constexpr (STATS) {
+        // |cards| - 1 summed over the wave's token-layers (each has at least one card)
+        const int64_t pf = static_cast<int64_t>(p) * a.F + f;
+        const uint32_t span = acc_span[q] - n_scored;
+        if (span) atomicAdd(&a.ws.acc_span_fam[pf], static_cast<unsigned long long>(span));
+        if (acc_cross[q]) atomicAdd(&a.ws.acc_cross_fam[pf], static_cast<unsigned long long>(acc_cross[q]));
+      }
     }
   }
   if (err) atomicOr(a.d_err, err);
   if (counter) {
     __syncthreads();
-    for (int i = threadIdx.x; i < E; i += blockDim.x)
-      if (ecnt[i]) atomicAdd(&a.ws.cnt[static_cast<int64_t>(l) * E + i], ecnt[i]);
+    for (int i = threadIdx.x; i < E; i += blockDim.x) {
+      if (ecnt[i]) {
+        atomicAdd(&a.ws.cnt[static_cast<int64_t>(l) * E + i], ecnt[i]);
+        if constexpr (STATS) atomicAdd(&a.ws.cnt_fam[(static_cast<int64_t>(f) * L + l) * E + i], ecnt[i]);
+      }
+    }
   }
 }
 
@@ -600,25 +657,60 @@ __global__ __launch_bounds__(256) void ev_finalize(EvArgs a, uint64_t* __restric
   }
 }
 
-template <int K, int PPL>
+// App. C statistics per (placement, family): home-family dispatch mass = dispatches of the family's
+// tokens to single-candidate experts whose primary lies in the family's band (from the per-family
+// dispatch counts) + replicated-slot choices inside the band (counted by ev_main).
+// grid (P, F), 256 threads.
+__global__ __launch_bounds__(256) void ev_stats(EvArgs a, uint64_t* __restrict__ span_fam,
+                                                uint64_t* __restrict__ cross_fam, uint64_t* __restrict__ hmass_fam) {
+  __shared__ unsigned long long red[4];
+  const int p = blockIdx.x, f = blockIdx.y;
+  const int E = a.E, L = a.L;
+  const uint4 r = a.band4[f >> 2];
+  const uint32_t bw = (f & 3) == 0 ? r.x : (f & 3) == 1 ? r.y : (f & 3) == 2 ? r.z : r.w;
+  const uint32_t hs = bw & 0xffu, hz = (bw >> 8) & 0xffu;
+  unsigned long long s = 0;
+  const int64_t n = static_cast<int64_t>(L) * E;
+  for (int64_t i = threadIdx.x; i < n; i += blockDim.x) {
+    if (a.ws.rep_of[i] != kNone) continue;
+    const uint32_t g = a.primary[static_cast<int64_t>(p) * n + i];
+    const int64_t le = i;  // (l, e) flattened
+    if (g - hs < hz) s += a.ws.cnt_fam[static_cast<int64_t>(f) * n + le];
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int64_t pf = static_cast<int64_t>(p) * a.F + f;
+    hmass_fam[pf] = red[0] + red[1] + red[2] + red[3] + a.ws.acc_hmass_fam[pf];
+    span_fam[pf] = a.ws.acc_span_fam[pf];
+    cross_fam[pf] = a.ws.acc_cross_fam[pf];
+  }
+}
+
+template <int K, int PPL, bool STATS>
 int launch_main(const EvArgs& a, int n_pblocks, hipStream_t stream) {
   constexpr int PW = 64 * PPL;
   const size_t lds = static_cast<size_t>(a.E) * PW * 4 + static_cast<size_t>(2) * TACG_MAX_REPLICATED * PW * 4 +
                      static_cast<size_t>(a.G) * PW * 2 + static_cast<size_t>(a.E) * 4 + align256(a.E);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&ev_main<K, PPL>), hipFuncAttributeMaxDynamicSharedMemorySize,
-                      static_cast<int>(lds));
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&ev_main<K, PPL, STATS>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
   EvArgs b = a;
   b.n_pblocks = n_pblocks;
   const int64_t grid = static_cast<int64_t>(n_pblocks) * a.n_pieces * a.L;
   if (grid > 0x7fffffff) return TACG_E_UNSUPPORTED;
-  hipLaunchKernelGGL((ev_main<K, PPL>), dim3(static_cast<uint32_t>(grid)), dim3(kMainThreads), lds, stream, b);
+  hipLaunchKernelGGL((ev_main<K, PPL, STATS>), dim3(static_cast<uint32_t>(grid)), dim3(kMainThreads), lds, stream,
+                     b);
   return TACG_OK;
 }
 
 template <int K>
 int launch_main_k(const EvArgs& a, hipStream_t stream) {
-  if (a.E > 64) return launch_main<K, 2>(a, (a.P + 127) / 128, stream);
-  return launch_main<K, 4>(a, (a.P + 255) / 256, stream);
+  // the statistics variant exists for two placements per lane only (it is not on the timed path)
+  if (a.stats) return launch_main<K, 2, true>(a, (a.P + 127) / 128, stream);
+  if (a.E > 64) return launch_main<K, 2, false>(a, (a.P + 127) / 128, stream);
+  return launch_main<K, 4, false>(a, (a.P + 255) / 256, stream);
 }
 
 // per-(placement, layer) primary-only loads from D.  grid (P, L), 256 threads.
@@ -694,7 +786,8 @@ int launch_eval(const int16_t* trace, int64_t N, int32_t L, int32_t K, int32_t E
                 int32_t F, const int32_t* home_start_host, const int32_t* home_size_host, int32_t G, int32_t P,
                 const uint8_t* primary, const uint8_t* secondary, int32_t R, const int64_t* load_ref,
                 int32_t theta_num, int32_t theta_den, uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
-                uint64_t* cost_home_fam, uint32_t* d_err, void* workspace, hipStream_t stream) {
+                uint64_t* cost_home_fam, const TraceStatsOut* stats, uint32_t* d_err, void* workspace,
+                hipStream_t stream) {
   EvArgs a{};
   a.trace = trace;
   a.primary = primary;
@@ -712,10 +805,17 @@ int launch_eval(const int16_t* trace, int64_t N, int32_t L, int32_t K, int32_t E
   a.R = R;
   a.theta_num = theta_num;
   a.theta_den = theta_den;
+  a.stats = stats != nullptr;
+  a.band_starts = stats != nullptr ? stats->band_starts : 0u;
+  for (int f = 0; f < F; ++f) {
+    const uint32_t bw = static_cast<uint32_t>(home_start_host[f]) | (static_cast<uint32_t>(home_size_host[f]) << 8);
+    uint4& r = a.band4[f >> 2];
+    ((f & 3) == 0 ? r.x : (f & 3) == 1 ? r.y : (f & 3) == 2 ? r.z : r.w) = bw;
+  }
   // pieces: split every family's tokens into chunks sized for about kTargetWorkgroups workgroups of
   // ev_main (at least 4096 tokens; at most 2^26 so that the per-lane 32-bit cost accumulators cannot
   // overflow).  Fewer, longer workgroups amortise the table set-up and the per-workgroup flushes.
-  const int64_t n_pblocks = E > 64 ? (P + 127) / 128 : (P + 255) / 256;
+  const int64_t n_pblocks = (E > 64 || stats != nullptr) ? (P + 127) / 128 : (P + 255) / 256;
   int64_t chunk = (N * n_pblocks * L + kTargetWorkgroups - 1) / kTargetWorkgroups;
   chunk = std::min<int64_t>(int64_t(1) << 26, std::max<int64_t>(4096, chunk));
   int np = 0;
@@ -769,6 +869,9 @@ int launch_eval(const int16_t* trace, int64_t N, int32_t L, int32_t K, int32_t E
     if (hipGetLastError() != hipSuccess) return TACG_E_DEVICE;
   }
   hipLaunchKernelGGL(ev_finalize, dim3(P, L), dim3(256), 0, stream, a, cost_home, cost_span, load, cost_home_fam);
+  if (stats != nullptr)
+    hipLaunchKernelGGL(ev_stats, dim3(P, F), dim3(256), 0, stream, a, stats->span_fam, stats->cross_fam,
+                       stats->home_mass_fam);
   return hipGetLastError() == hipSuccess ? TACG_OK : TACG_E_DEVICE;
 }
 

@@ -48,6 +48,14 @@ int launch_pair_jaccard(const uint32_t* C, int32_t n_fam, int32_t n_layers, int3
                         int32_t* top_pairs, double* jaccard, hipStream_t stream);
 
 // ---- placement scoring ---------------------------------------------------------------------
+// Optional App. C statistics of the snapshot scoring (all pointers device memory, [P][F]).
+struct TraceStatsOut {
+  uint64_t* span_fam;
+  uint64_t* cross_fam;
+  uint64_t* home_mass_fam;
+  uint32_t band_starts;  // bit b set when a family band starts at GPU b (the bands tile 0..G-1)
+};
+
 size_t eval_workspace(int64_t n_tokens, int32_t n_layers, int32_t n_experts, int32_t n_gpus, int32_t n_place,
                       int32_t n_fam);
 int launch_eval(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
@@ -55,7 +63,8 @@ int launch_eval(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_
                 const int32_t* home_size_host, int32_t n_gpus, int32_t n_place, const uint8_t* primary,
                 const uint8_t* secondary, int32_t n_sec, const int64_t* load_ref, int32_t theta_num,
                 int32_t theta_den, uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
-                uint64_t* cost_home_fam, uint32_t* d_err, void* workspace, hipStream_t stream);
+                uint64_t* cost_home_fam, const TraceStatsOut* stats, uint32_t* d_err, void* workspace,
+                hipStream_t stream);
 int launch_eval_online(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
                        const int64_t* fam_off_host, int32_t n_fam, const int32_t* home_start_host,
                        const int32_t* home_size_host, int32_t n_gpus, int32_t n_place, const uint8_t* primary,

@@ -127,6 +127,30 @@ def test_eval_argument_errors(L):
     assert call(off_=np.array([0, 60, 90], dtype=np.int64)) == tacg.E_INVAL
 
 
+def test_eval_trace_stats_argument_errors(L):
+    off = np.array([0, 60, 100], dtype=np.int64)
+    hs = np.array([0, 2], dtype=np.int32)
+    hz = np.array([2, 2], dtype=np.int32)
+
+    def call(G=4, P=3, hs_=hs, hz_=hz, flags=0, wsb=1 << 30, sf=FAKE, cf=FAKE, mf=FAKE):
+        return L.tacg_eval_trace_stats(FAKE, 100, 2, 2, 8, off.ctypes.data_as(ctypes.c_void_p), 2,
+                                       hs_.ctypes.data_as(ctypes.c_void_p), hz_.ctypes.data_as(ctypes.c_void_p),
+                                       G, P, FAKE, None, 0, None, 3, 20, FAKE, FAKE, FAKE, sf, cf, mf, flags, FAKE,
+                                       FAKE, wsb, None)
+
+    assert call(G=33) == tacg.E_UNSUPPORTED
+    assert call(P=0) == tacg.E_INVAL
+    assert call(flags=1) == tacg.E_INVAL
+    assert call(wsb=1) == tacg.E_INVAL
+    assert call(sf=None) == tacg.E_INVAL
+    assert call(cf=None) == tacg.E_INVAL
+    assert call(mf=None) == tacg.E_INVAL
+    # the distinct family bands must tile the GPUs: overlapping bands, or a GPU outside every band
+    assert call(hs_=np.array([0, 1], dtype=np.int32), hz_=np.array([2, 3], dtype=np.int32)) == tacg.E_UNSUPPORTED
+    assert call(hs_=np.array([0, 0], dtype=np.int32), hz_=np.array([2, 2], dtype=np.int32)) == tacg.E_UNSUPPORTED
+    assert call(hs_=np.array([0, 0], dtype=np.int32), hz_=np.array([2, 4], dtype=np.int32)) == tacg.E_UNSUPPORTED
+
+
 def test_eval_online_argument_errors(L):
     off = np.array([0, 60, 100], dtype=np.int64)
     hs = np.array([0, 2], dtype=np.int32)
