@@ -23,6 +23,9 @@ namespace tacg {
 namespace {
 
 constexpr int kReduceThreads = 1024;
+constexpr int kCoactSmallE = 128;        // at most this many experts: the small-triangle launch
+constexpr int kCoactThreadsLarge = 1024;  // threads per histogram workgroup, E > kCoactSmallE
+constexpr int kCoactThreadsSmall = 512;   // threads per histogram workgroup, E <= kCoactSmallE
 constexpr int kDepth = 4;  // token-layers per thread in flight in coact_hist_kernel
 
 struct CoactArgs {
@@ -161,8 +164,8 @@ __device__ __forceinline__ void count_token(const RawIds<K>& raw, bool valid, ui
   }
 }
 
-template <int K>
-__global__ __launch_bounds__(kCoactThreads) void coact_hist_kernel(CoactArgs a) {
+template <int K, int THREADS>
+__global__ __launch_bounds__(THREADS) void coact_hist_kernel(CoactArgs a) {
   extern __shared__ uint32_t hist[];
   const int tid = threadIdx.x;
   const int nb = a.nbins;
@@ -272,11 +275,17 @@ __global__ __launch_bounds__(kReduceThreads) void coact_reduce_kernel(CoactArgs 
   }
 }
 
+template <int K, int THREADS>
+void launch_hist_t(const CoactArgs& a, size_t lds, hipStream_t stream) {
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&coact_hist_kernel<K, THREADS>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  hipLaunchKernelGGL((coact_hist_kernel<K, THREADS>), dim3(a.W), dim3(THREADS), lds, stream, a);
+}
+
 template <int K>
 void launch_hist(const CoactArgs& a, size_t lds, hipStream_t stream) {
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&coact_hist_kernel<K>),
-                      hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-  hipLaunchKernelGGL(coact_hist_kernel<K>, dim3(a.W), dim3(kCoactThreads), lds, stream, a);
+  if (a.E > kCoactSmallE) launch_hist_t<K, kCoactThreadsLarge>(a, lds, stream);
+  else launch_hist_t<K, kCoactThreadsSmall>(a, lds, stream);
 }
 
 }  // namespace
@@ -287,8 +296,9 @@ size_t coact_bins(int32_t n_experts, int32_t top_k) {
 }
 
 int coact_num_workgroups(int64_t total, int32_t n_experts) {
-  // one workgroup per CU when the triangle needs more than half of the 160 KB LDS, else two
-  const int64_t cap = (n_experts > 128) ? 256 : 512;
+  // E > 128: the triangle needs more than half of the 160 KB LDS, so one 1024-thread workgroup per
+  // CU; otherwise four 512-thread workgroups per CU (the same 32 waves, with four private triangles)
+  const int64_t cap = (n_experts > kCoactSmallE) ? 256 : 1024;
   const int64_t want = (total + 32767) / 32768;
   return static_cast<int>(std::max<int64_t>(1, std::min(cap, want)));
 }

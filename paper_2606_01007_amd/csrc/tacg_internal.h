@@ -25,7 +25,6 @@ struct Carver {
 };
 
 // ---- co-activation build -------------------------------------------------------------------
-constexpr int kCoactThreads = 1024;
 int coact_num_workgroups(int64_t total_token_layers, int32_t n_experts);
 size_t coact_bins(int32_t n_experts, int32_t top_k);
 
