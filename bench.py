@@ -225,7 +225,9 @@ def main():
     trace_bytes_s = Ns * L * k * 2
     c_bytes = F * L * E * E * 4 + F * L * E * 4
     coact_gbs = (trace_bytes_g + c_bytes) / t_coact / 1e9
-    valu_ops = ptl * ((k - 1) + 3)                     # k-1 ORs of one-hot GPU masks, andn, 2 popcounts
+    # algorithmic integer work per placement-token-layer: k table lookups, k-1 ORs of one-hot GPU masks,
+    # two popcounts and the replica resolution, about 2k + 6 lane-ops
+    valu_ops = ptl * (2 * k + 6)
     eval_tops = valu_ops / t_eval / 1e12
     result = {
         "metric": METRIC,
@@ -260,8 +262,10 @@ def main():
                      "achieved": eval_tops, "peak": VALU_PEAK_TOPS, "unit": "TFLOP/s",
                      "frac": eval_tops / VALU_PEAK_TOPS,
                      "traffic": None if reduced else measured_traffic("ev_main", cfg.name),
-                     "note": "int32 lane-ops per placement-token-layer: k-1 ORs of one-hot GPU masks, "
-                             "one and-not and two popcounts; peak = 256 CUs x 64 lanes x 2.4 GHz"},
+                     "note": "2k + 6 int32 lane-ops per placement-token-layer (k table lookups, k-1 ORs "
+                             "of one-hot GPU masks, two popcounts, replica resolution); the stricter "
+                             "k + 2 count (ORs, and-not, popcounts only) gives frac x (k+2)/(2k+6); "
+                             "peak = 256 CUs x 64 lanes x 2.4 GHz"},
         "roofline_coact": {"kernel": "coact_hist + coact_reduce (tacg_coact_build)", "bound": "hbm",
                            "achieved": coact_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": coact_gbs / HBM_PEAK_GBS,
