@@ -33,7 +33,7 @@ size_t tacg_coact_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t to
                                   int32_t n_fam) {
   if (n_tokens < 0 || n_layers < 1 || top_k < 1 || n_experts < 1 || n_fam < 1) return 0;
   const int64_t total = n_tokens * n_layers;
-  const int64_t W = tacg::coact_num_workgroups(total, n_experts);
+  const int64_t W = tacg::coact_num_workgroups(total, n_experts, top_k);
   const size_t slots = static_cast<size_t>(W) + static_cast<size_t>(n_layers) * n_fam;
   return tacg::align256(slots * tacg::coact_bins(n_experts, top_k) * sizeof(uint32_t));
 }

@@ -17,6 +17,8 @@
 //     workspace (slot indices are unique because both w and s grow along x), then zeroes it.
 //   * A second kernel, one workgroup per segment, sums the partial slots of the workgroups that
 //     touched the segment and writes the dense symmetric C (diagonal = D) and D.
+//   * At E <= 64 and k >= 5 the partial slots come from int8 matrix products instead
+//     (coact_mfma.hip), with the same split of x, the same slots and the same reduction.
 #include "tacg_internal.h"
 
 namespace tacg {
@@ -204,7 +206,7 @@ __global__ __launch_bounds__(THREADS) void coact_hist_kernel(CoactArgs a) {
         ring[d].fetch(a.trace + min(x + kDepth * bd, last) * K);
       }
     }
-    __syncthreads();
+    barrier_after_lds_atomics();
     uint32_t* dst = a.partial + (w + l * a.F + f) * static_cast<int64_t>(nb);
     for (int i = tid; i < nb; i += blockDim.x) {
       dst[i] = hist[i];
@@ -295,7 +297,8 @@ size_t coact_bins(int32_t n_experts, int32_t top_k) {
   return static_cast<size_t>(n_experts) * static_cast<size_t>(n_experts - 1) / 2;
 }
 
-int coact_num_workgroups(int64_t total, int32_t n_experts) {
+int coact_num_workgroups(int64_t total, int32_t n_experts, int32_t top_k) {
+  if (coact_uses_mfma(n_experts, top_k)) return coact_mfma_workgroups(total);
   // E > 128: the triangle needs more than half of the 160 KB LDS, so one 1024-thread workgroup per
   // CU; otherwise four 512-thread workgroups per CU (the same 32 waves, with four private triangles)
   const int64_t cap = (n_experts > kCoactSmallE) ? 256 : 1024;
@@ -314,13 +317,17 @@ int launch_coact(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32
   a.K = top_k;
   a.E = n_experts;
   a.F = n_fam;
-  a.W = coact_num_workgroups(a.total, n_experts);
+  a.W = coact_num_workgroups(a.total, n_experts, top_k);
   a.nbins = static_cast<int32_t>(coact_bins(n_experts, top_k));
   a.partial = static_cast<uint32_t*>(workspace);
   a.d_err = d_err;
   for (int f = 0; f <= n_fam; ++f) a.fam_off[f] = fam_off_host[f];
   const size_t lds = static_cast<size_t>(a.nbins) * sizeof(uint32_t);
-  if (a.total > 0) {
+  if (a.total > 0 && coact_uses_mfma(n_experts, top_k)) {
+    const int rc = launch_coact_mfma_hist(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, a.W,
+                                          a.nbins, a.partial, d_err, stream);
+    if (rc != TACG_OK) return rc;
+  } else if (a.total > 0) {
     switch (top_k) {
 #define TACG_K(k) \
   case k:         \

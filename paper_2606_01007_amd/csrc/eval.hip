@@ -171,7 +171,7 @@ __global__ __launch_bounds__(256) void ev_replist(EvArgs a) {
     }
     a.ws.rep_of[static_cast<int64_t>(l) * a.E + e] = r;
   }
-  __syncthreads();
+  barrier_after_lds_atomics();
   if (e == 0) {
     a.ws.n_rep[l] = min(cnt, TACG_MAX_REPLICATED);
     if (cnt > TACG_MAX_REPLICATED) atomicOr(a.d_err, TACG_ERR_LIMIT);
@@ -470,7 +470,7 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
       }
     }
     if (nrep > 0) {  // fold the 16-bit choice counters of this round into registers (nrep is workgroup-uniform)
-      __syncthreads();
+      barrier_after_lds_atomics();
 #pragma unroll
       for (int c = 0; c < kRcntPerThread; ++c) {
         const int i = threadIdx.x + c * kMainThreads;
@@ -616,7 +616,7 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
   }
   if (err) atomicOr(a.d_err, err);
   if (counter) {
-    __syncthreads();
+    barrier_after_lds_atomics();
     for (int i = threadIdx.x; i < E; i += blockDim.x) {
       if (ecnt[i]) {
         atomicAdd(&a.ws.cnt[static_cast<int64_t>(l) * E + i], ecnt[i]);
@@ -641,7 +641,7 @@ __global__ __launch_bounds__(256) void ev_finalize(EvArgs a, uint64_t* __restric
     const uint32_t c = a.ws.cnt[static_cast<int64_t>(l) * E + e];
     if (g < G && c) atomicAdd(&acc[g], c);
   }
-  __syncthreads();
+  barrier_after_lds_atomics();
   if (threadIdx.x < G) {
     const int64_t o = (static_cast<int64_t>(p) * L + l) * G + threadIdx.x;
     load[o] = acc[threadIdx.x] + a.ws.rep_load[o];
@@ -732,7 +732,7 @@ __global__ __launch_bounds__(256) void placement_load_kernel(const uint32_t* __r
     for (int f = 0; f < F; ++f) s += D[(static_cast<int64_t>(f) * L + l) * E + e];
     if (s) atomicAdd(&acc[g], s);
   }
-  __syncthreads();
+  barrier_after_lds_atomics();
   if (threadIdx.x < G) load_ref[(static_cast<int64_t>(p) * L + l) * G + threadIdx.x] = static_cast<int64_t>(acc[threadIdx.x]);
   if (err) atomicOr(d_err, err);
 }

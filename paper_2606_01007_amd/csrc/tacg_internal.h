@@ -12,6 +12,15 @@ namespace tacg {
 // Round a byte count up to the 256-byte alignment used for every workspace sub-buffer.
 inline size_t align256(size_t x) { return (x + 255u) & ~size_t(255); }
 
+// Workgroup barrier after LDS counters were incremented with relaxed atomics by several waves: first
+// wait until this wave's LDS operations have completed (s_waitcnt lgkmcnt(0)), then synchronise.
+// The compiler does not always emit that wait before the barrier after relaxed LDS atomics; without
+// it a wave's last increments can land after another wave has read (and cleared) the counters.
+__device__ __forceinline__ void barrier_after_lds_atomics() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0); vmcnt and expcnt at their maxima (no wait)
+  __syncthreads();
+}
+
 // Bump allocator over a caller-provided workspace (device memory).  Only carves offsets.
 struct Carver {
   char* base;
@@ -25,8 +34,14 @@ struct Carver {
 };
 
 // ---- co-activation build -------------------------------------------------------------------
-int coact_num_workgroups(int64_t total_token_layers, int32_t n_experts);
+int coact_num_workgroups(int64_t total_token_layers, int32_t n_experts, int32_t top_k);
 size_t coact_bins(int32_t n_experts, int32_t top_k);
+// small expert counts: the counts come from int8 matrix products (coact_mfma.hip)
+bool coact_uses_mfma(int32_t n_experts, int32_t top_k);
+int coact_mfma_workgroups(int64_t total_token_layers);
+int launch_coact_mfma_hist(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
+                           int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam, int32_t W, int32_t nbins,
+                           uint32_t* partial, uint32_t* d_err, hipStream_t stream);
 
 int launch_coact(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
                  const int64_t* fam_off_host, int32_t n_fam, uint32_t* D, uint32_t* C, uint32_t flags,

@@ -119,26 +119,44 @@ def test_coact_repeat_is_deterministic():
     assert torch.equal(D1, D2) and torch.equal(C1, C2)
 
 
-def test_coact_data_errors_flagged():
-    E, k = 16, 4
+@pytest.mark.parametrize("E,k,counts,L", [(8, 2, [2048, 2048, 2048], 2), (100, 4, [300, 0, 513, 7], 3),
+                                           (256, 8, [600, 1, 900], 2), (13, 1, [700, 300], 2),
+                                           (48, 7, [900, 0, 1500, 65], 2)])
+def test_coact_repeated_builds_exact(E, k, counts, L):
+    """Many short segments flush the workgroup triangles often; every one of repeated builds into the
+    same outputs must equal the oracle (a lost or late increment at a flush would show here)."""
+    _say(f"coact repeated E={E} k={k} counts={counts} L={L}")
+    off = synth.fam_offsets(counts)
+    tr = _rand_trace(L, int(off[-1]), k, E, 77)
+    Do, Co, _ = oracle.coact(tr.cpu(), off, E)
+    D, C, err = tacg.coact_build(tr, off, E)
+    for _ in range(12):
+        tacg.coact_build(tr, off, E, D=D, C=C, err=err)
+        np.testing.assert_array_equal(_u32(C), Co)
+        np.testing.assert_array_equal(_u32(D), Do)
+    assert _err(err) == 0
+
+
+@pytest.mark.parametrize("E,k", [(16, 4), (16, 6), (200, 8)])   # histogram, matrix-core, histogram paths
+def test_coact_data_errors_flagged(E, k):
+    """Repeated and out-of-range ids are flagged; the offending token-layer is skipped, as the oracle
+    skips it."""
     tr = _rand_trace(1, 3000, k, E, 13)
-    bad = tr.clone()
-    bad[0, 100, 1] = bad[0, 100, 0]
-    _, _, err = tacg.coact_build(bad, [0, 3000], E)
-    assert _err(err) & tacg.ERR_ID_DUP
-    bad = tr.clone()
-    bad[0, 7, 3] = E
-    _, _, err = tacg.coact_build(bad, [0, 3000], E)
-    assert _err(err) & tacg.ERR_ID_RANGE
-    bad = tr.clone()
-    bad[0, 9, 2] = -3
-    _, _, err = tacg.coact_build(bad, [0, 3000], E)
-    assert _err(err) & tacg.ERR_ID_RANGE
+    for t, s, v, bit in [(100, 1, None, tacg.ERR_ID_DUP), (7, 3, E, tacg.ERR_ID_RANGE), (9, 2, -3, tacg.ERR_ID_RANGE)]:
+        bad = tr.clone()
+        bad[0, t, s] = bad[0, t, 0] if v is None else v
+        D, C, err = tacg.coact_build(bad, [0, 3000], E)
+        assert _err(err) & bit
+        Do, Co, eo = oracle.coact(bad.cpu(), [0, 3000], E)
+        assert eo & bit
+        np.testing.assert_array_equal(_u32(C), Co)
+        np.testing.assert_array_equal(_u32(D), Do)
 
 
-def test_coact_empty_trace():
-    tr = torch.zeros((2, 0, 4), dtype=torch.int16, device="cuda")
-    D, C, err = tacg.coact_build(tr, [0, 0, 0], 16)
+@pytest.mark.parametrize("E,k", [(16, 4), (16, 6)])
+def test_coact_empty_trace(E, k):
+    tr = torch.zeros((2, 0, k), dtype=torch.int16, device="cuda")
+    D, C, err = tacg.coact_build(tr, [0, 0, 0], E)
     assert _err(err) == 0
     assert int(D.abs().sum()) == 0 and int(C.abs().sum()) == 0
 
