@@ -153,13 +153,36 @@ __device__ __forceinline__ void count_token(const RawIds<K>& raw, bool valid, ui
       uint32_t rb[K - 1];
 #pragma unroll
       for (int i = 0; i < K - 1; ++i) rb[i] = __umul24(v[i], rbk - 2u * v[i]) - 4u;
+      if constexpr (K >= 6 && K <= 8) {
+        // Odd lanes increment their pairs in the reverse order.  A pair that is frequent in a family
+        // tends to sit at the same place in the sorted pair lists of many tokens, and lanes that add to
+        // one address in the same instruction are serialised; reversing half the lanes splits those
+        // collisions (measured on MI355X at top-8: 10 % faster at E = 128, 2 % at E = 256; at top-4 the
+        // extra selects cost more than they save).
+        constexpr int NP = K * (K - 1) / 2;
+        uint32_t off[NP];
+        int n = 0;
 #pragma unroll
-      for (int i = 0; i < K - 1; ++i) {
+        for (int i = 0; i < K - 1; ++i) {
 #pragma unroll
-        for (int j = i + 1; j < K; ++j) {
-          uint32_t* cell = reinterpret_cast<uint32_t*>(
-              __builtin_assume_aligned(reinterpret_cast<char*>(hist) + (rb[i] + 4u * v[j]), 4));
+          for (int j = i + 1; j < K; ++j) off[n++] = rb[i] + 4u * v[j];
+        }
+        const bool odd = (threadIdx.x & 1u) != 0u;
+#pragma unroll
+        for (int q = 0; q < NP; ++q) {
+          uint32_t* cell = reinterpret_cast<uint32_t*>(__builtin_assume_aligned(
+              reinterpret_cast<char*>(hist) + (odd ? off[NP - 1 - q] : off[q]), 4));
           __hip_atomic_fetch_add(cell, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < K - 1; ++i) {
+#pragma unroll
+          for (int j = i + 1; j < K; ++j) {
+            uint32_t* cell = reinterpret_cast<uint32_t*>(
+                __builtin_assume_aligned(reinterpret_cast<char*>(hist) + (rb[i] + 4u * v[j]), 4));
+            __hip_atomic_fetch_add(cell, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          }
         }
       }
     }
@@ -226,8 +249,12 @@ __device__ __forceinline__ int64_t owner_of(int64_t x, int64_t total, int64_t W)
 // One workgroup per segment s = l * F + f.  The partial triangles of the workgroups that touched
 // the segment are summed into LDS with coalesced reads; then each wave writes dense rows i of C
 // (lanes over columns j, coalesced) from the LDS triangle and recovers D_i from the row sum.
+// Both phases are branch-free in their inner loops (indices are clamped and the values selected),
+// so every load of a thread is in flight before the first wait: one workgroup fills a CU, and the
+// HBM latency has to be covered by the loads of its own threads.
+template <bool ACC, int NQ>  // NQ = ceil(E / 64) columns per lane
 __global__ __launch_bounds__(kReduceThreads) void coact_reduce_kernel(CoactArgs a, uint32_t* __restrict__ D,
-                                                                      uint32_t* __restrict__ C, uint32_t accumulate) {
+                                                                      uint32_t* __restrict__ C) {
   extern __shared__ uint32_t tri[];
   const int s = blockIdx.x;
   const int l = s / a.F, f = s % a.F;
@@ -239,41 +266,81 @@ __global__ __launch_bounds__(kReduceThreads) void coact_reduce_kernel(CoactArgs 
     w0 = owner_of(seg0, a.total, a.W);
     w1 = owner_of(seg1 - 1, a.total, a.W);
   }
-  const int nb = a.nbins;
-  for (int b = threadIdx.x; b < nb; b += blockDim.x) {
-    uint32_t v = 0;
-    for (int64_t w = w0; w <= w1; ++w) v += __builtin_nontemporal_load(&a.partial[(w + s) * static_cast<int64_t>(nb) + b]);
-    tri[b] = v;
+  const int nb = a.nbins;  // >= 1
+  constexpr int kUnroll = 4 * NQ;  // about nbins / kReduceThreads loads per thread
+  for (int b0 = threadIdx.x; b0 < nb; b0 += kUnroll * kReduceThreads) {
+    uint32_t v[kUnroll] = {};
+    for (int64_t w = w0; w <= w1; ++w) {
+      const uint32_t* src = a.partial + (w + s) * static_cast<int64_t>(nb);
+      uint32_t x[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) x[u] = __builtin_nontemporal_load(src + min(b0 + u * kReduceThreads, nb - 1));
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) v[u] += x[u];
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int b = b0 + u * kReduceThreads;
+      if (b < nb) tri[b] = v[u];
+    }
   }
   __syncthreads();
 
-  const int lane = threadIdx.x & 63;
+  const uint32_t lane = threadIdx.x & 63u;
   const int wave = threadIdx.x >> 6;
-  const int nwaves = blockDim.x >> 6;
+  constexpr int nwaves = kReduceThreads / 64;
+  const uint32_t ue = static_cast<uint32_t>(E);
+  const uint32_t rk = 2u * ue - 3u;
+  const bool pairs = a.K > 1;
   uint32_t* Dseg = D + (static_cast<int64_t>(f) * a.L + l) * E;
   uint32_t* Cseg = C + (static_cast<int64_t>(f) * a.L + l) * E * static_cast<int64_t>(E);
   for (int i = wave; i < E; i += nwaves) {
-    uint32_t rowsum = 0;
+    const uint32_t ui = static_cast<uint32_t>(i);
     uint32_t* crow = Cseg + static_cast<int64_t>(i) * E;
-    for (int j = lane; j < E; j += 64) {
-      if (j == i) continue;  // the diagonal is written below, from the row sum
-      uint32_t v = 0;
-      if (a.K > 1) {
-        const uint32_t lo = min(i, j), hi = max(i, j);
-        v = tri[lo * (2u * E - 3u - lo) / 2u - 1u + hi];
-        rowsum += v;
-      }
-      crow[j] = accumulate ? crow[j] + v : v;
+    uint32_t val[NQ];
+    uint32_t rowsum = 0;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const uint32_t j = lane + 64u * q;
+      const uint32_t lo = min(ui, j), hi = max(ui, j);
+      const bool off = pairs && j < ue && j != ui;
+      const uint32_t x = tri[off ? lo * (rk - lo) / 2u - 1u + hi : 0u];
+      val[q] = off ? x : 0u;
+      rowsum += val[q];
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) rowsum += __shfl_xor(rowsum, o, 64);
-    if (lane == 0) {
-      // each valid token with expert i adds k - 1 pairs to row i; with k = 1 the bins are D itself
-      const uint32_t d = (a.K == 1) ? tri[i] : rowsum / static_cast<uint32_t>(a.K - 1);
-      const uint32_t dn = accumulate ? Dseg[i] + d : d;
-      Dseg[i] = dn;
-      crow[i] = dn;
+    // each valid token with expert i adds k - 1 pairs to row i; with k = 1 the bins are D itself
+    const uint32_t d = pairs ? rowsum / static_cast<uint32_t>(a.K - 1) : tri[i];
+    const uint32_t dn = ACC ? Dseg[i] + d : d;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const uint32_t j = lane + 64u * q;
+      if (j < ue) {
+        uint32_t out = (j == ui) ? dn : val[q];
+        if (ACC && j != ui) out += crow[j];
+        crow[j] = out;
+      }
     }
+    if (lane == 0) Dseg[i] = dn;
+  }
+}
+
+template <bool ACC, int NQ>
+void launch_reduce_t(const CoactArgs& a, dim3 grid, size_t lds, uint32_t* D, uint32_t* C, hipStream_t stream) {
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&coact_reduce_kernel<ACC, NQ>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  hipLaunchKernelGGL((coact_reduce_kernel<ACC, NQ>), grid, dim3(kReduceThreads), lds, stream, a, D, C);
+}
+
+template <bool ACC>
+void launch_reduce(const CoactArgs& a, int nq, dim3 grid, size_t lds, uint32_t* D, uint32_t* C, hipStream_t stream) {
+  static_assert(TACG_MAX_EXPERTS <= 4 * 64, "one to four column chunks per lane");
+  switch (nq) {
+    case 1: launch_reduce_t<ACC, 1>(a, grid, lds, D, C, stream); break;
+    case 2: launch_reduce_t<ACC, 2>(a, grid, lds, D, C, stream); break;
+    case 3: launch_reduce_t<ACC, 3>(a, grid, lds, D, C, stream); break;
+    default: launch_reduce_t<ACC, 4>(a, grid, lds, D, C, stream); break;
   }
 }
 
@@ -342,10 +409,12 @@ int launch_coact(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32
     if (hipGetLastError() != hipSuccess) return TACG_E_DEVICE;
   }
   if (a.total == 0) a.total = 1;  // the reduction sees no contributors (all segments empty)
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&coact_reduce_kernel),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-  hipLaunchKernelGGL(coact_reduce_kernel, dim3(n_layers * n_fam), dim3(kReduceThreads), lds, stream, a, D, C,
-                     (flags & TACG_ACCUMULATE) ? 1u : 0u);
+  const int nq = (n_experts + 63) / 64;
+  if (flags & TACG_ACCUMULATE) {
+    launch_reduce<true>(a, nq, dim3(n_layers * n_fam), lds, D, C, stream);
+  } else {
+    launch_reduce<false>(a, nq, dim3(n_layers * n_fam), lds, D, C, stream);
+  }
   if (hipGetLastError() != hipSuccess) return TACG_E_DEVICE;
   return TACG_OK;
 }

@@ -64,6 +64,8 @@ def _rand_trace(L, N, k, E, seed, device="cuda"):
     (256, 16, 1, [2000], 8),
     (200, 3, 3, [4000, 4000], 9),
     (32, 12, 2, [1500, 500], 10),
+    (100, 6, 2, [2500, 1700], 11),
+    (129, 7, 3, [999, 3001], 12),
 ])
 def test_coact_parity(E, k, L, counts, seed):
     _say(f"coact E={E} k={k} L={L} counts={counts}")
@@ -121,7 +123,7 @@ def test_coact_repeat_is_deterministic():
 
 @pytest.mark.parametrize("E,k,counts,L", [(8, 2, [2048, 2048, 2048], 2), (100, 4, [300, 0, 513, 7], 3),
                                            (256, 8, [600, 1, 900], 2), (13, 1, [700, 300], 2),
-                                           (48, 7, [900, 0, 1500, 65], 2)])
+                                           (48, 7, [900, 0, 1500, 65], 2), (90, 6, [800, 77, 1200], 2)])
 def test_coact_repeated_builds_exact(E, k, counts, L):
     """Many short segments flush the workgroup triangles often; every one of repeated builds into the
     same outputs must equal the oracle (a lost or late increment at a flush would show here)."""
