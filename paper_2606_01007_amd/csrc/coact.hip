@@ -154,11 +154,12 @@ __device__ __forceinline__ void count_token(const RawIds<K>& raw, bool valid, ui
 #pragma unroll
       for (int i = 0; i < K - 1; ++i) rb[i] = __umul24(v[i], rbk - 2u * v[i]) - 4u;
       if constexpr (K >= 6 && K <= 8) {
-        // Odd lanes increment their pairs in the reverse order.  A pair that is frequent in a family
-        // tends to sit at the same place in the sorted pair lists of many tokens, and lanes that add to
-        // one address in the same instruction are serialised; reversing half the lanes splits those
-        // collisions (measured on MI355X at top-8: 10 % faster at E = 128, 2 % at E = 256; at top-4 the
-        // extra selects cost more than they save).
+        // Lanes walk their pair lists in one of four orders (lane bit 0: reversed, bit 1: rotated by
+        // half the list).  A pair that is frequent in a family tends to sit at the same place in the
+        // sorted pair lists of many tokens, and lanes that add to one address in the same instruction
+        // are serialised; the four orders split those collisions.  Measured on MI355X at top-8 against
+        // one order: 1.68 -> 1.42 ms at E = 128 (48 layers x 2^22 tokens), 3.38 -> 3.16 ms at E = 256;
+        // eight orders gained nothing more, and at top-4 the selects cost more than they save.
         constexpr int NP = K * (K - 1) / 2;
         uint32_t off[NP];
         int n = 0;
@@ -167,11 +168,15 @@ __device__ __forceinline__ void count_token(const RawIds<K>& raw, bool valid, ui
 #pragma unroll
           for (int j = i + 1; j < K; ++j) off[n++] = rb[i] + 4u * v[j];
         }
-        const bool odd = (threadIdx.x & 1u) != 0u;
+        const bool rev = (threadIdx.x & 1u) != 0u;
+        const bool rot = (threadIdx.x & 2u) != 0u;
 #pragma unroll
         for (int q = 0; q < NP; ++q) {
+          const int q2 = (q + NP / 2) % NP;
+          const uint32_t x = rev ? off[NP - 1 - q] : off[q];
+          const uint32_t y = rev ? off[NP - 1 - q2] : off[q2];
           uint32_t* cell = reinterpret_cast<uint32_t*>(__builtin_assume_aligned(
-              reinterpret_cast<char*>(hist) + (odd ? off[NP - 1 - q] : off[q]), 4));
+              reinterpret_cast<char*>(hist) + (rot ? y : x), 4));
           __hip_atomic_fetch_add(cell, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
       } else {
