@@ -6,17 +6,21 @@
 // theta_num) * S with S = L_0 + L_1 + ... + L_31 summed in that order (GPUs >= G hold +0.0).
 //
 // Kernel design (gfx950): the scan over tokens is sequential, the (placement, layer) scans are
-// independent.  Lane = placement, wave = 64 placements of one layer, one wave per workgroup.
-//   * LDS holds, for the wave's placements, every expert's primary GPU (pg[e][lane], one byte), the
-//     candidate masks of the experts that have a secondary in any of these placements (rm[r][lane],
-//     up to kRepLds of them; rix[e] maps an expert to its row, and the rare experts beyond that
-//     read their tables from memory), and per-lane dispatch counters (cnt[m][lane]).  About 36 KB at
-//     E = 256, so four waves share a CU and all P * L / 64 waves are resident at once.
+// independent.  Lane = placement, wave = 64 placements of one layer, one wave per workgroup, so there
+// is about one wave per SIMD and nothing hides a latency on the per-token chain: the token loop keeps
+// LDS off that chain.
+//   * LDS holds one code byte per (expert, lane): the GPU of an expert with a single candidate in the
+//     lane's placement, else 32 + the row of its candidate mask in rm (rows shared by the wave's
+//     placements; code 63 when the rows ran out and the mask is read from the tables).  The k codes of
+//     a token are read one token ahead, so their latency overlaps the previous token's work.
 //   * The wave loads 64 token-layers at once (one per lane), packs their ids and a word with the
 //     validity, family and anchor position, and broadcasts them token by token with v_readlane.
-//   * The loads live in 32 float64 registers per lane.  The per-token dispatch counts Delta are kept
-//     as packed 4-bit fields (8-bit fields for top-k = 16) so that every GPU's fused multiply-add
-//     reads its count with one bit-field extract.
+//   * The loads live in float64 registers (8 or 32 per lane, by G).  The per-token dispatch counts
+//     Delta are packed 4-bit fields in 64-bit words (8-bit fields for top-k = 16), one shift-add per
+//     slot, one bit-field extract per GPU in the fused multiply-adds.
+//   * Per-GPU dispatch totals: the wave also counts every expert's valid dispatches of its layer
+//     (ecnt, in the per-tile preparation); at the end each lane adds ecnt[e] to the GPU of every
+//     single-candidate expert, and only the choices of multi-candidate slots are counted per token.
 #include "tacg_internal.h"
 
 namespace tacg {
@@ -25,7 +29,6 @@ namespace {
 constexpr int kLanes = 64;
 constexpr uint8_t kNone = 0xFF;
 constexpr uint8_t kOver = 0xFE;  // replicated expert without an LDS row (read from memory)
-constexpr int kRepLds = 48;      // candidate-mask rows in LDS per workgroup
 
 struct OnArgs {
   const int16_t* trace;
@@ -59,26 +62,30 @@ __global__ __launch_bounds__(256) void on_zero(OnArgs a) {
     for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.F; j += stride) a.cost_home_fam[j] = 0;
 }
 
-// Per-token dispatch counts of the 32 GPUs, packed: 4-bit fields when at most 15 slots can land on
-// one GPU, else 8-bit fields.
-template <bool kWide>
+// Per-token dispatch counts of GPUs 0 .. NG-1, packed in 64-bit words: 4-bit fields when at most 15
+// slots can land on one GPU, else 8-bit fields.  add(g) with g >= NG (a multi-candidate code) adds
+// nothing.
+template <bool kWide, int NG>
 struct Delta {
   static constexpr int kBits = kWide ? 8 : 4;
-  static constexpr int kPerWord = 32 / kBits;
-  static constexpr int kWords = 32 / kPerWord;
-  uint32_t w[kWords];
+  static constexpr int kPerWord = 64 / kBits;
+  static constexpr int kWords = (NG + kPerWord - 1) / kPerWord;
+  uint64_t w[kWords];
   __device__ __forceinline__ void clear() {
 #pragma unroll
     for (int i = 0; i < kWords; ++i) w[i] = 0;
   }
   __device__ __forceinline__ void add(uint32_t g) {
-    const uint32_t inc = 1u << (kBits * (g % kPerWord));
+    const uint64_t inc = 1ull << ((kBits * g) & 63u);
     const uint32_t word = g / kPerWord;
 #pragma unroll
-    for (int i = 0; i < kWords; ++i) w[i] += (word == static_cast<uint32_t>(i)) ? inc : 0u;
+    for (int i = 0; i < kWords; ++i) w[i] += (word == static_cast<uint32_t>(i)) ? inc : 0ull;
   }
   __device__ __forceinline__ uint32_t get(int m) const {
-    return __builtin_amdgcn_ubfe(w[m / kPerWord], kBits * (m % kPerWord), kBits);
+    const uint64_t x = w[m / kPerWord];
+    const int sh = kBits * (m % kPerWord);
+    const uint32_t half = sh < 32 ? static_cast<uint32_t>(x) : static_cast<uint32_t>(x >> 32);
+    return __builtin_amdgcn_ubfe(half, sh & 31, kBits);
   }
 };
 
@@ -109,43 +116,26 @@ __device__ __forceinline__ uint32_t candidate_mask(const OnArgs& a, bool live, i
   return m ? m : 1u;
 }
 
-// Candidate mask of expert e for this lane: its LDS row, or the tables themselves for an expert
-// beyond the LDS rows.
-__device__ __forceinline__ uint32_t slot_mask(const OnArgs& a, const uint32_t* rm, const uint8_t* rix, uint32_t e,
-                                              bool live, int64_t base, int lane) {
-  const uint8_t r = rix[e];
-  if (r != kOver) return rm[r * kLanes + lane];
-  uint32_t unused = 0;
-  return candidate_mask(a, live, base + e, unused);
-}
+typedef uint32_t v32u __attribute__((ext_vector_type(32)));
 
-// argmin over the GPUs of fc of the loads, ties to the lowest number, as a balanced tree of pairwise
-// minima (the left, lower-numbered operand wins ties, so the result is the sequential argmin)
-__device__ __forceinline__ uint32_t least_loaded(const double (&Lm)[32], uint32_t fc) {
-  double v[16];
-  uint32_t ix[16];
-#pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const double a0 = ((fc >> (2 * i)) & 1u) ? Lm[2 * i] : __builtin_inf();
-    const double a1 = ((fc >> (2 * i + 1)) & 1u) ? Lm[2 * i + 1] : __builtin_inf();
-    const bool right = a1 < a0;
-    v[i] = right ? a1 : a0;
-    ix[i] = right ? 2u * i + 1u : 2u * i;
-  }
-#pragma unroll
-  for (int w = 8; w >= 1; w >>= 1) {
-#pragma unroll
-    for (int i = 0; i < w; ++i) {
-      const bool right = v[2 * i + 1] < v[2 * i];
-      v[i] = right ? v[2 * i + 1] : v[2 * i];
-      ix[i] = right ? ix[2 * i + 1] : ix[2 * i];
-    }
-  }
-  return ix[0];
-}
+constexpr int kRows = 31;           // candidate-mask rows in LDS per workgroup (codes 32 .. 62)
+constexpr uint32_t kCodeOver = 63;  // multi-candidate expert without a row: read its tables
+constexpr int kMaxCand = TACG_MAX_SECONDARY + 1;
 
-// grid (ceil(P / 64), L), 64 threads.
-template <int K>
+// The lane's code bytes of experts 0 .. 255 in 64 registers (two 32-register vectors).  The expert id
+// of a lookup is wave-uniform, so the lookup is an indexed register move (s_set_gpr_idx) and not a
+// memory access.
+struct CodeRegs {
+  v32u lo, hi;
+  __device__ __forceinline__ uint32_t get(uint32_t e) const {
+    const uint32_t i = (e >> 2) & 31u;
+    const uint32_t w = e < 128u ? lo[i] : hi[i];
+    return __builtin_amdgcn_ubfe(w, 8u * (e & 3u), 8u);
+  }
+};
+
+// grid (ceil(P / 64), L), 64 threads; NG = 8 or 32 >= G GPUs in registers.
+template <int K, int NG>
 __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
   extern __shared__ __align__(16) uint32_t lds[];
   constexpr int KB = (K + 3) / 4;  // dwords of 8-bit ids per token-layer
@@ -154,38 +144,56 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
   const int p = blockIdx.x * kLanes + lane;
   const bool live = p < a.P;
   const int E = a.E, G = a.G, L = a.L;
-  uint32_t* rm = lds;                                                  // [kRepLds][64] candidate masks
-  uint32_t* cnt = rm + kRepLds * kLanes;                               // [32][64] dispatch counters
-  uint8_t* pg = reinterpret_cast<uint8_t*>(cnt + 32 * kLanes);          // [E][64] primary GPUs
-  uint8_t* rix = pg + E * kLanes;                                      // [E] row of rm, kNone or kOver
+  uint32_t* rm = lds;                                            // [kRows][64] candidate masks
+  uint32_t* cnt = rm + kRows * kLanes;                           // [32][64] dispatches per GPU
+  uint32_t* ecnt = cnt + 32 * kLanes;                            // [E] valid dispatches per expert
+  // shared region: the code bytes [E][64] while the tables are read, then this lane's loads [NG][64]
+  // (float64) whenever a token has multi-candidate slots
+  uint8_t* code = reinterpret_cast<uint8_t*>(ecnt + TACG_MAX_EXPERTS);
+  double* Lc = reinterpret_cast<double*>(code);
   uint32_t err = 0;
 
   // ---- candidate sets of this lane's placement (eq. candidate-set) ----
   const int64_t base = (static_cast<int64_t>(p) * L + l) * E;
   int nr = 0;  // rows of rm in use (workgroup-uniform)
-  for (int e = 0; e < E; ++e) {
-    const uint32_t m = candidate_mask(a, live, base + e, err);
-    pg[e * kLanes + lane] = static_cast<uint8_t>(find_first_bit(m));
-    const bool multi = __popc(m) > 1;
-    uint8_t r = kNone;
-    if (__ballot(multi)) {
-      if (nr < kRepLds) {
-        rm[nr * kLanes + lane] = m;
-        r = static_cast<uint8_t>(nr++);
-      } else {
-        r = kOver;
+  for (int e = 0; e < TACG_MAX_EXPERTS; ++e) {
+    uint32_t c = 0;
+    if (e < E) {
+      const uint32_t m = candidate_mask(a, live, base + e, err);
+      const bool multi = __popc(m) > 1;
+      c = find_first_bit(m);
+      if (__ballot(multi)) {
+        if (nr < kRows) {
+          rm[nr * kLanes + lane] = m;
+          if (multi) c = 32u + static_cast<uint32_t>(nr);
+          ++nr;
+        } else if (multi) {
+          c = kCodeOver;
+        }
       }
     }
-    if (lane == 0) rix[e] = r;
+    code[e * kLanes + lane] = static_cast<uint8_t>(c);
+  }
+  CodeRegs cr;
+#pragma unroll
+  for (int i = 0; i < 64; ++i) {
+    const uint32_t w = static_cast<uint32_t>(code[(4 * i) * kLanes + lane]) |
+                       (static_cast<uint32_t>(code[(4 * i + 1) * kLanes + lane]) << 8) |
+                       (static_cast<uint32_t>(code[(4 * i + 2) * kLanes + lane]) << 16) |
+                       (static_cast<uint32_t>(code[(4 * i + 3) * kLanes + lane]) << 24);
+    if (i < 32) cr.lo[i] = w;
+    else cr.hi[i - 32] = w;
   }
 #pragma unroll
   for (int m = 0; m < 32; ++m) cnt[m * kLanes + lane] = 0;
-  __syncthreads();
+  for (int e = lane; e < E; e += kLanes) ecnt[e] = 0;
+  __syncthreads();  // the code bytes are in registers; the region now holds the loads
 
-  double Lm[32];
+  double Lm[NG];
 #pragma unroll
-  for (int m = 0; m < 32; ++m) Lm[m] = (a.state_in && live && m < G) ? a.state_in[(base / E) * G + m] : 0.0;
+  for (int m = 0; m < NG; ++m) Lm[m] = (a.state_in && live && m < G) ? a.state_in[(base / E) * G + m] : 0.0;
   const double rho = a.rho;
+  const bool guard = a.theta_den != 0;
   const double gden = static_cast<double>(a.theta_den) * static_cast<double>(G);
   const double rnum = static_cast<double>(a.theta_den) + static_cast<double>(a.theta_num);
 
@@ -215,10 +223,14 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
         for (int q = 0; q < s; ++q) dup |= raw[s] == raw[q];
         const uint32_t id = min(raw[s], static_cast<uint32_t>(E - 1));
         pk[s >> 2] |= id << (8 * (s & 3));
-        if (rix[id] != kNone) info |= 1u << (16 + s);  // an expert with several candidates somewhere
       }
       if (!ok) err |= TACG_ERR_ID_RANGE;
       if (dup) err |= TACG_ERR_ID_DUP;
+      if (ok && !dup) {
+#pragma unroll
+        for (int s = 0; s < K; ++s)
+          __hip_atomic_fetch_add(&ecnt[raw[s]], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
       int f = f_tile;
       while (static_cast<int64_t>(a.fam[f].y) <= t) ++f;
       const uint4 fr = a.fam[f];
@@ -227,6 +239,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
       info |= ((ok && !dup) ? 1u : 0u) | (static_cast<uint32_t>(f) << 1) | (pos << 8);
     }
     const int ntile = static_cast<int>(min(static_cast<int64_t>(kLanes), a.N - tile));
+
     for (int j = 0; j < ntile; ++j) {
       const uint32_t tinfo = __builtin_amdgcn_readlane(info, j);
       if (!(tinfo & 1u)) continue;  // invalid token-layer (flagged): not served
@@ -243,43 +256,38 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
       const uint32_t h = (a.fam[f].z & 0xffu) + ((tinfo >> 8) & 0xffu);
 
       // single-candidate slots first: they form the set R of GPUs the token reaches
-      Delta<(K > 15)> dl;
+      uint32_t c[K];
+#pragma unroll
+      for (int s = 0; s < K; ++s) c[s] = cr.get(__builtin_amdgcn_ubfe(ids[s >> 2], 8 * (s & 3), 8));
+      Delta<(K > 15), NG> dl;
       dl.clear();
       uint32_t R = 0, pend = 0;
 #pragma unroll
       for (int s = 0; s < K; ++s) {
-        const uint32_t e = __builtin_amdgcn_ubfe(ids[s >> 2], 8 * (s & 3), 8);
-        uint32_t g;
-        if ((tinfo >> (16 + s)) & 1u) {  // workgroup-uniform: e has several candidates somewhere
-          const uint32_t c = slot_mask(a, rm, rix, e, live, base, lane);
-          if (__popc(c) > 1) {
-            pend |= 1u << s;
-            continue;
-          }
-          g = find_first_bit(c);
-        } else {
-          g = pg[e * kLanes + lane];
-        }
-        R |= 1u << g;
-        dl.add(g);
-        __hip_atomic_fetch_add(&cnt[g * kLanes + lane], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        const bool single = c[s] < 32u;
+        R |= single ? (1u << c[s]) : 0u;
+        pend |= single ? 0u : (1u << s);
+        dl.add(c[s]);
       }
       if (__ballot(pend != 0)) {
-        // feasible GPUs under the current loads (eq. feasible-set with the mean of eq. mean-load)
-        uint32_t feas = 0xffffffffu;
-        if (a.theta_den != 0) {
+        // the guard's right-hand side under the current loads (eq. feasible-set with the mean of
+        // eq. mean-load), and the loads in LDS so that a slot reads those of its own candidates
+        double rhs = 0.0;
+        if (guard) {
           double S = 0.0;
 #pragma unroll
-          for (int m = 0; m < 32; ++m) S += Lm[m];
-          const double rhs = rnum * S;
-          feas = 0;
-#pragma unroll
-          for (int m = 0; m < 32; ++m) feas |= (gden * Lm[m] <= rhs) ? (1u << m) : 0u;
+          for (int m = 0; m < NG; ++m) S += Lm[m];
+          rhs = rnum * S;
         }
+#pragma unroll
+        for (int m = 0; m < NG; ++m) Lc[m * kLanes + lane] = Lm[m];
         // multi-candidate slots in slot order: a reached feasible candidate (lowest number), else
         // the anchor if feasible, else the least-loaded feasible candidate (ties: lowest number).
-        // The slot loop stays rolled so that the 32-GPU scan below exists once and indexes the loads
-        // statically; the slot's id comes out of two 64-bit words by a shift.
+        uint64_t cw[(K + 7) / 8];
+#pragma unroll
+        for (int q = 0; q < (K + 7) / 8; ++q) cw[q] = 0;
+#pragma unroll
+        for (int s = 0; s < K; ++s) cw[s >> 3] |= static_cast<uint64_t>(c[s]) << (8 * (s & 7));
         const uint64_t id_lo = static_cast<uint64_t>(ids[0]) | (KB > 1 ? static_cast<uint64_t>(ids[KB > 1 ? 1 : 0]) << 32 : 0);
         const uint64_t id_hi = KB > 2 ? (static_cast<uint64_t>(ids[KB > 2 ? 2 : 0]) |
                                          (KB > 3 ? static_cast<uint64_t>(ids[KB > 3 ? 3 : 0]) << 32 : 0))
@@ -287,18 +295,52 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
 #pragma unroll 1
         for (int s = 0; s < K; ++s) {
           if (!((pend >> s) & 1u)) continue;
-          const uint64_t wd = s < 8 ? id_lo : id_hi;
-          const uint32_t e = static_cast<uint32_t>(wd >> (8 * (s & 7))) & 0xffu;
-          const uint32_t c = slot_mask(a, rm, rix, e, live, base, lane);
-          uint32_t fc = c & feas;
-          if (!fc) fc = c;
+          const uint32_t cs = static_cast<uint32_t>(cw[s >> 3] >> (8 * (s & 7))) & 0xffu;
+          uint32_t cm;
+          if (cs != kCodeOver) {
+            cm = rm[(cs - 32u) * kLanes + lane];
+          } else {
+            const uint64_t wd = s < 8 ? id_lo : id_hi;
+            const uint32_t e = static_cast<uint32_t>(wd >> (8 * (s & 7))) & 0xffu;
+            uint32_t unused = 0;
+            cm = candidate_mask(a, live, base + e, unused);
+          }
+          // the candidates in increasing GPU order (at most kMaxCand) and their loads
+          const int ncand = __popc(cm);
+          uint32_t g[kMaxCand];
+          double v[kMaxCand];
+          uint32_t rest = cm;
+#pragma unroll
+          for (int i = 0; i < kMaxCand; ++i) {
+            g[i] = min(find_first_bit(rest), static_cast<uint32_t>(NG - 1));  // ffbl(0) = ~0: unused
+            rest &= rest - 1u;
+            v[i] = Lc[g[i] * kLanes + lane];
+          }
+          uint32_t fc = cm;
+          if (guard) {
+            uint32_t feas = 0;
+#pragma unroll
+            for (int i = 0; i < kMaxCand; ++i) feas |= (i < ncand && gden * v[i] <= rhs) ? (1u << g[i]) : 0u;
+            fc = feas ? feas : cm;
+          }
           uint32_t pick;
           if (fc & R) {
             pick = find_first_bit(fc & R);
           } else if ((fc >> h) & 1u) {
             pick = h;
           } else {
-            pick = least_loaded(Lm, fc);
+            // least loaded in fc; candidates come in increasing GPU order, so a strict < keeps
+            // the lowest number among equal loads
+            pick = 32u;
+            double best = 0.0;
+#pragma unroll
+            for (int i = 0; i < kMaxCand; ++i) {
+              const bool in = i < ncand && ((fc >> g[i]) & 1u);
+              if (in && (pick == 32u || v[i] < best)) {
+                best = v[i];
+                pick = g[i];
+              }
+            }
           }
           R |= 1u << pick;
           dl.add(pick);
@@ -312,9 +354,19 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
       fam_acc += home;
       // eq. load-update after the token's dispatch
 #pragma unroll
-      for (int m = 0; m < 32; ++m) Lm[m] = __fma_rn(rho, Lm[m], static_cast<double>(dl.get(m)));
+      for (int m = 0; m < NG; ++m) Lm[m] = __fma_rn(rho, Lm[m], static_cast<double>(dl.get(m)));
     }
   }
+
+  // dispatches of the single-candidate experts: every valid dispatch of e goes to its one GPU
+  barrier_after_lds_atomics();
+  for (int e = 0; e < E; ++e) {
+    const uint32_t cs = cr.get(static_cast<uint32_t>(e));
+    const uint32_t ne = ecnt[e];
+    if (cs < 32u && ne)
+      __hip_atomic_fetch_add(&cnt[cs * kLanes + lane], ne, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  barrier_after_lds_atomics();
 
   if (live) {
     if (cur_f >= 0 && a.cost_home_fam && fam_acc)
@@ -325,20 +377,27 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
     for (int m = 0; m < G; ++m) a.load[o + m] = cnt[m * kLanes + lane];
     if (a.state_out) {
 #pragma unroll
-      for (int m = 0; m < 32; ++m)  // static register indices: the loads never leave registers
+      for (int m = 0; m < NG; ++m)  // static register indices: the loads never leave registers
         if (m < G) a.state_out[o + m] = Lm[m];
     }
   }
   if (err) atomicOr(a.d_err, err);
 }
 
+template <int K, int NG>
+void launch_on_t(const OnArgs& a, hipStream_t stream) {
+  // candidate rows, counters, expert counts, then the larger of the code bytes and the loads
+  const size_t lds = (static_cast<size_t>(kRows) * kLanes + 32 * kLanes + TACG_MAX_EXPERTS) * sizeof(uint32_t) +
+                     std::max(static_cast<size_t>(TACG_MAX_EXPERTS) * kLanes, static_cast<size_t>(NG) * kLanes * 8);
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&on_main<K, NG>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+  hipLaunchKernelGGL((on_main<K, NG>), dim3((a.P + kLanes - 1) / kLanes, a.L), dim3(kLanes), lds, stream, a);
+}
+
 template <int K>
 void launch_on(const OnArgs& a, hipStream_t stream) {
-  const size_t lds = (static_cast<size_t>(kRepLds) * kLanes + 32 * kLanes) * sizeof(uint32_t) +
-                     static_cast<size_t>(a.E) * kLanes + static_cast<size_t>(a.E);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&on_main<K>), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            static_cast<int>(lds));
-  hipLaunchKernelGGL(on_main<K>, dim3((a.P + kLanes - 1) / kLanes, a.L), dim3(kLanes), lds, stream, a);
+  if (a.G <= 8) launch_on_t<K, 8>(a, stream);
+  else launch_on_t<K, 32>(a, stream);
 }
 
 }  // namespace
