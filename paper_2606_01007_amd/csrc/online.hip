@@ -147,15 +147,18 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
   uint32_t* rm = lds;                                            // [kRows][64] candidate masks
   uint32_t* cnt = rm + kRows * kLanes;                           // [32][64] dispatches per GPU
   uint32_t* ecnt = cnt + 32 * kLanes;                            // [E] valid dispatches per expert
-  // shared region: the code bytes [E][64] while the tables are read, then this lane's loads [NG][64]
-  // (float64) whenever a token has multi-candidate slots
-  uint8_t* code = reinterpret_cast<uint8_t*>(ecnt + TACG_MAX_EXPERTS);
-  double* Lc = reinterpret_cast<double*>(code);
+  uint32_t* hasrow = ecnt + TACG_MAX_EXPERTS;                    // [8] experts with several candidates somewhere
+  // shared region: the code bytes [E][64] while the tables are read, then this lane's loads as pairs
+  // [NG / 2][64] of float64 whenever a token has multi-candidate slots
+  uint8_t* code = reinterpret_cast<uint8_t*>(hasrow + 8);
+  double2* Lc2 = reinterpret_cast<double2*>(code);
+  const double* Lc = reinterpret_cast<const double*>(code);
   uint32_t err = 0;
 
   // ---- candidate sets of this lane's placement (eq. candidate-set) ----
   const int64_t base = (static_cast<int64_t>(p) * L + l) * E;
   int nr = 0;  // rows of rm in use (workgroup-uniform)
+  if (lane < 8) hasrow[lane] = 0;
   for (int e = 0; e < TACG_MAX_EXPERTS; ++e) {
     uint32_t c = 0;
     if (e < E) {
@@ -163,6 +166,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
       const bool multi = __popc(m) > 1;
       c = find_first_bit(m);
       if (__ballot(multi)) {
+        if (lane == 0) hasrow[e >> 5] |= 1u << (e & 31);
         if (nr < kRows) {
           rm[nr * kLanes + lane] = m;
           if (multi) c = 32u + static_cast<uint32_t>(nr);
@@ -223,6 +227,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
         for (int q = 0; q < s; ++q) dup |= raw[s] == raw[q];
         const uint32_t id = min(raw[s], static_cast<uint32_t>(E - 1));
         pk[s >> 2] |= id << (8 * (s & 3));
+        info |= ((hasrow[id >> 5] >> (id & 31)) & 1u) << (16 + s);  // a candidate row exists for id
       }
       if (!ok) err |= TACG_ERR_ID_RANGE;
       if (dup) err |= TACG_ERR_ID_DUP;
@@ -269,7 +274,9 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
         pend |= single ? 0u : (1u << s);
         dl.add(c[s]);
       }
-      if (__ballot(pend != 0)) {
+      // slots whose expert has several candidates in some placement of the wave (wave-uniform)
+      const uint32_t pend_any = tinfo >> 16;
+      if (pend_any) {
         // the guard's right-hand side under the current loads (eq. feasible-set with the mean of
         // eq. mean-load), and the loads in LDS so that a slot reads those of its own candidates
         double rhs = 0.0;
@@ -280,9 +287,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
           rhs = rnum * S;
         }
 #pragma unroll
-        for (int m = 0; m < NG; ++m) Lc[m * kLanes + lane] = Lm[m];
-        // multi-candidate slots in slot order: a reached feasible candidate (lowest number), else
-        // the anchor if feasible, else the least-loaded feasible candidate (ties: lowest number).
+        for (int m = 0; m < NG; m += 2) Lc2[(m >> 1) * kLanes + lane] = make_double2(Lm[m], Lm[m + 1]);
         uint64_t cw[(K + 7) / 8];
 #pragma unroll
         for (int q = 0; q < (K + 7) / 8; ++q) cw[q] = 0;
@@ -292,18 +297,24 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
         const uint64_t id_hi = KB > 2 ? (static_cast<uint64_t>(ids[KB > 2 ? 2 : 0]) |
                                          (KB > 3 ? static_cast<uint64_t>(ids[KB > 3 ? 3 : 0]) << 32 : 0))
                                       : 0;
-#pragma unroll 1
-        for (int s = 0; s < K; ++s) {
-          if (!((pend >> s) & 1u)) continue;
+        // multi-candidate slots in slot order: a reached feasible candidate (lowest number), else
+        // the anchor if feasible, else the least-loaded feasible candidate (ties: lowest number).
+        // The loop visits the wave's candidate slots only; a lane whose placement has a single
+        // candidate for that slot takes no part.
+        for (uint32_t rem = pend_any; rem != 0u; rem &= rem - 1u) {
+          const int s = __builtin_ctz(rem);
+          const bool active = (pend >> s) & 1u;
           const uint32_t cs = static_cast<uint32_t>(cw[s >> 3] >> (8 * (s & 7))) & 0xffu;
-          uint32_t cm;
-          if (cs != kCodeOver) {
-            cm = rm[(cs - 32u) * kLanes + lane];
-          } else {
-            const uint64_t wd = s < 8 ? id_lo : id_hi;
-            const uint32_t e = static_cast<uint32_t>(wd >> (8 * (s & 7))) & 0xffu;
-            uint32_t unused = 0;
-            cm = candidate_mask(a, live, base + e, unused);
+          uint32_t cm = 1u;
+          if (active) {
+            if (cs != kCodeOver) {
+              cm = rm[(cs - 32u) * kLanes + lane];
+            } else {
+              const uint64_t wd = s < 8 ? id_lo : id_hi;
+              const uint32_t e = static_cast<uint32_t>(wd >> (8 * (s & 7))) & 0xffu;
+              uint32_t unused = 0;
+              cm = candidate_mask(a, live, base + e, unused);
+            }
           }
           // the candidates in increasing GPU order (at most kMaxCand) and their loads
           const int ncand = __popc(cm);
@@ -314,7 +325,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
           for (int i = 0; i < kMaxCand; ++i) {
             g[i] = min(find_first_bit(rest), static_cast<uint32_t>(NG - 1));  // ffbl(0) = ~0: unused
             rest &= rest - 1u;
-            v[i] = Lc[g[i] * kLanes + lane];
+            v[i] = Lc[((g[i] >> 1) * kLanes + lane) * 2 + (g[i] & 1u)];
           }
           uint32_t fc = cm;
           if (guard) {
@@ -323,28 +334,25 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
             for (int i = 0; i < kMaxCand; ++i) feas |= (i < ncand && gden * v[i] <= rhs) ? (1u << g[i]) : 0u;
             fc = feas ? feas : cm;
           }
-          uint32_t pick;
-          if (fc & R) {
-            pick = find_first_bit(fc & R);
-          } else if ((fc >> h) & 1u) {
-            pick = h;
-          } else {
-            // least loaded in fc; candidates come in increasing GPU order, so a strict < keeps
-            // the lowest number among equal loads
-            pick = 32u;
-            double best = 0.0;
+          // least loaded in fc; candidates come in increasing GPU order, so a strict < keeps the
+          // lowest number among equal loads
+          uint32_t least = g[0];
+          double best = 0.0;
+          bool found = false;
 #pragma unroll
-            for (int i = 0; i < kMaxCand; ++i) {
-              const bool in = i < ncand && ((fc >> g[i]) & 1u);
-              if (in && (pick == 32u || v[i] < best)) {
-                best = v[i];
-                pick = g[i];
-              }
-            }
+          for (int i = 0; i < kMaxCand; ++i) {
+            const bool in = i < ncand && ((fc >> g[i]) & 1u);
+            const bool better = in && (!found || v[i] < best);
+            best = better ? v[i] : best;
+            least = better ? g[i] : least;
+            found |= in;
           }
-          R |= 1u << pick;
-          dl.add(pick);
-          __hip_atomic_fetch_add(&cnt[pick * kLanes + lane], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          const uint32_t fr = fc & R;
+          const uint32_t pick = fr ? find_first_bit(fr) : (((fc >> h) & 1u) ? h : least);
+          R |= active ? (1u << pick) : 0u;
+          dl.add(active ? pick : 63u);
+          if (active)
+            __hip_atomic_fetch_add(&cnt[pick * kLanes + lane], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
       }
       const uint32_t n = __popc(R);
@@ -387,7 +395,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
 template <int K, int NG>
 void launch_on_t(const OnArgs& a, hipStream_t stream) {
   // candidate rows, counters, expert counts, then the larger of the code bytes and the loads
-  const size_t lds = (static_cast<size_t>(kRows) * kLanes + 32 * kLanes + TACG_MAX_EXPERTS) * sizeof(uint32_t) +
+  const size_t lds = (static_cast<size_t>(kRows) * kLanes + 32 * kLanes + TACG_MAX_EXPERTS + 8) * sizeof(uint32_t) +
                      std::max(static_cast<size_t>(TACG_MAX_EXPERTS) * kLanes, static_cast<size_t>(NG) * kLanes * 8);
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&on_main<K, NG>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
