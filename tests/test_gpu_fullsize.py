@@ -1,5 +1,6 @@
 """GPU parity at the full workload sizes (the preset shapes at their full token, layer and placement
-counts, in the launch configuration the benchmark times).
+counts, in the launch configuration the benchmark times; the decayed-load scoring on the benchmark's
+sample of the serving trace, its first 2^19 tokens).
 
 The oracle computes sampled outputs one by one (a few family/layer segments of the counts, the
 reweighted graph of sampled layers, a few scored placements over the whole trace); every other
@@ -115,3 +116,30 @@ def test_full_size(name):
             np.testing.assert_allclose(float(jn[p]), jo[0], rtol=1e-5)
             np.testing.assert_allclose(float(mv[p]), vo[0], rtol=1e-5, atol=1e-30)
     _say(f"[{name}] scoring ok")
+
+    # ---- decayed-load scoring on the benchmark's sample: all placements, sampled ones vs the oracle ----
+    ps = w.placement_sets[0]
+    G, P = ps["n_gpus"], ps["primary"].shape[0]
+    n = min(1 << 19, w.trace_serve.shape[1])
+    tr = w.trace_serve[:, :n].contiguous()
+    off = np.minimum(np.asarray(w.fam_off_serve, dtype=np.int64), n)
+    prim = torch.as_tensor(ps["primary"]).cuda()
+    sec = torch.as_tensor(ps["secondary"]).cuda() if ps["secondary"] is not None else None
+    on = tacg.eval_online(tr, off, E, ps["home_start"], ps["home_size"], G, prim, sec, rho=0.995, theta=(3, 20))
+    torch.cuda.synchronize()
+    assert int(on["err"].item()) == 0
+    load = _u32(on["load"])
+    assert bool((load.sum(dim=2) == n * k).all())
+    assert torch.equal(on["cost_home_fam"].sum(dim=1), on["cost_home"])
+    tsn = np.ascontiguousarray(ts[:, :n])
+    for p in sorted({0, P // 2, P - 1}):
+        _say(f"[{name}] oracle decayed-load scoring placement {p} of {P} (G={G}, {n} tokens)")
+        ro = oracle.score_online(tsn, off, E, ps["home_start"], ps["home_size"], G, ps["primary"], ps["secondary"],
+                                 rho=0.995, theta=(3, 20), p_range=(p, p + 1))
+        assert ro["err"] == 0
+        assert int(on["cost_home"][p]) == int(ro["cost_home"][p])
+        assert int(on["cost_span"][p]) == int(ro["cost_span"][p])
+        np.testing.assert_array_equal(load[p].cpu().numpy(), ro["load"][p])
+        np.testing.assert_array_equal(on["cost_home_fam"][p].cpu().numpy(), ro["cost_home_fam"][p])
+        np.testing.assert_array_equal(on["state"][p].cpu().numpy(), ro["state"][p])
+    _say(f"[{name}] decayed-load scoring ok")
