@@ -5,7 +5,7 @@
 //
 // dist_kernel: one workgroup per family pair, layers in sequence, float64.
 // top_pairs_kernel: one workgroup per (family, layer).  The segment's upper triangle is staged in
-//   LDS (130,560 B at E = 256), the n-th largest positive count T is found by bisection on counts,
+//   LDS (130,560 B at E = 256; rows by waves, coalesced), the n-th largest positive count T is found by bisection on counts,
 //   pairs above T are kept, ties at T are kept in increasing pair order until n are chosen (a
 //   chunked block scan gives each tie its rank), and the chosen pairs are written in increasing pair
 //   order (a second scan gives each its slot).
@@ -96,13 +96,36 @@ __global__ __launch_bounds__(kTopThreads) void top_pairs_kernel(const uint32_t* 
   const uint32_t UE = static_cast<uint32_t>(E);
   const uint32_t npairs = UE * (UE - 1u) / 2u;
   const uint32_t* seg = C + (static_cast<int64_t>(f) * L + l) * E * static_cast<int64_t>(E);
-  for (int idx = tid; idx < E * E; idx += nt) {
-    const uint32_t a = idx / E, b = idx % E;
-    if (a < b) tri[tri_index(a, b, UE)] = seg[idx];
+  // stage the strict upper triangle row by row: each wave takes rows, lanes take columns; four rows
+  // per step, all their loads in flight (addresses clamped into the segment, stores only for a < b)
+  {
+    const int lane = tid & 63, wave = tid >> 6, nw = nt >> 6;
+    for (int a0 = wave; a0 < E; a0 += 4 * nw) {
+      uint32_t v[4][4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int a = min(a0 + r * nw, E - 1);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[r][q] = seg[a * E + min(a + 1 + lane + 64 * q, E - 1)];
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int a = a0 + r * nw;
+        if (a < E) {
+          const uint32_t base = tri_index(static_cast<uint32_t>(a), static_cast<uint32_t>(a) + 1u, UE);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int b = a + 1 + lane + 64 * q;
+            if (b < E) tri[base + static_cast<uint32_t>(b - a - 1)] = v[r][q];
+          }
+        }
+      }
+    }
   }
   __syncthreads();
-  // this thread's contiguous chunk of the triangle
-  const uint32_t per = (npairs + nt - 1) / nt;
+  // this thread's contiguous chunk of the triangle; an odd chunk length puts the 32 threads of a
+  // half-wave on 32 different LDS banks at every step of the chunk scans
+  const uint32_t per = ((npairs + nt - 1) / nt) | 1u;
   const uint32_t t0 = min(npairs, tid * per), t1 = min(npairs, t0 + per);
   // largest count
   uint32_t mx = 0;
