@@ -63,14 +63,6 @@ __device__ double block_sum(double v, double* red) {
   return t;
 }
 
-// tokens of family f at layer l: sum_i D[f][l][i] / k
-__device__ double family_tokens(const uint32_t* D, int f, int l, int L, int E, int k) {
-  const uint32_t* d = D + (static_cast<int64_t>(f) * L + l) * E;
-  uint64_t s = 0;
-  for (int i = 0; i < E; ++i) s += d[i];
-  return static_cast<double>(s) / k;
-}
-
 // N_f of every (layer, family): one wave per pair, lanes over experts (an exact integer sum); the
 // (l, 0) wave also clears the layer's maximum.
 __global__ __launch_bounds__(64) void rw_nf(const uint32_t* __restrict__ D, int F, int L, int E, int k, RwWs ws) {
@@ -231,28 +223,55 @@ __global__ __launch_bounds__(256) void rw_graph(int F, int L, int E, double alph
 // GESR identification scores (Sec. 3.4, eq. generic-score) per row i of layer l, float64:
 // Cent = sum_j A-bar(i, j); Cons = mean_f cos(A_f(i, :), A-bar(i, :)) (0 for a zero row);
 // Spec = max_f ||A_f(i, :) - A-bar(i, :)||_2.  One wave per row, lanes over columns; the family rows
-// are read twice (once for A-bar, once for the per-family terms).  grid (L, row blocks), 256 threads.
+// are read twice (once for A-bar, once for the per-family terms), eight families' rows in flight at a
+// time.  grid (L, row blocks), 256 threads.
 __global__ __launch_bounds__(256) void gesr_scores_kernel(const uint32_t* __restrict__ D,
                                                           const uint32_t* __restrict__ C, int F, int L, int E, int k,
                                                           double* __restrict__ cent, double* __restrict__ cons,
                                                           double* __restrict__ spec) {
   __shared__ double inv_n[TACG_MAX_FAMILIES];
   const int l = blockIdx.x;
-  if (threadIdx.x < F) {
-    const double n = family_tokens(D, threadIdx.x, l, L, E, k);
-    inv_n[threadIdx.x] = n > 0 ? 1.0 / n : 0.0;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  // N_f of the layer: one wave per family, an exact integer sum over the experts
+  for (int f = wave; f < F; f += nw) {
+    const uint32_t* d = D + (static_cast<int64_t>(f) * L + l) * E;
+    unsigned long long t = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = lane + 64 * q;
+      if (e < E) t += d[e];
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) t += __shfl_xor(t, o, 64);
+    const double n = static_cast<double>(t) / k;
+    if (lane == 0) inv_n[f] = n > 0 ? 1.0 / n : 0.0;
   }
   __syncthreads();
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const int r0 = blockIdx.y * kRows, r1 = min(E, r0 + kRows);
-  for (int i = r0 + wave; i < r1; i += nw) {
-    double ab[4] = {0, 0, 0, 0};
-    for (int f = 0; f < F; ++f) {
+  // the rows of families f0 .. f0 + 7 of row i (family index clamped into range)
+  auto load_rows = [&](int i, int f0, uint32_t (&v)[kFamChunk][4]) {
+#pragma unroll
+    for (int u = 0; u < kFamChunk; ++u) {
+      const int f = min(f0 + u, F - 1);
       const uint32_t* row = C + ((static_cast<int64_t>(f) * L + l) * E + i) * E;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int j = lane + 64 * q;
-        if (j < E && j != i) ab[q] += row[j] * inv_n[f];
+      for (int q = 0; q < 4; ++q) v[u][q] = row[min(lane + 64 * q, E - 1)];
+    }
+  };
+  for (int i = r0 + wave; i < r1; i += nw) {
+    double ab[4] = {0, 0, 0, 0};
+    for (int f0 = 0; f0 < F; f0 += kFamChunk) {
+      uint32_t v[kFamChunk][4];
+      load_rows(i, f0, v);
+#pragma unroll
+      for (int u = 0; u < kFamChunk; ++u) {
+        const int f = f0 + u;
+        if (f >= F) break;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int j = lane + 64 * q;
+          if (j < E && j != i) ab[q] += v[u][q] * inv_n[f];
+        }
       }
     }
     double cs = 0.0, nb2 = 0.0;
@@ -266,25 +285,31 @@ __global__ __launch_bounds__(256) void gesr_scores_kernel(const uint32_t* __rest
     nb2 = wave_sum(nb2);
     const double nb = sqrt(nb2);
     double cos_sum = 0.0, worst = 0.0;
-    for (int f = 0; f < F; ++f) {
-      const uint32_t* row = C + ((static_cast<int64_t>(f) * L + l) * E + i) * E;
-      double dot = 0.0, na2 = 0.0, dev2 = 0.0;
+    for (int f0 = 0; f0 < F; f0 += kFamChunk) {
+      uint32_t v[kFamChunk][4];
+      load_rows(i, f0, v);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int j = lane + 64 * q;
-        if (j < E) {
-          const double a = (j != i) ? row[j] * inv_n[f] : 0.0;
-          dot += a * ab[q];
-          na2 += a * a;
-          dev2 += (a - ab[q]) * (a - ab[q]);
+      for (int u = 0; u < kFamChunk; ++u) {
+        const int f = f0 + u;
+        if (f >= F) break;
+        double dot = 0.0, na2 = 0.0, dev2 = 0.0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int j = lane + 64 * q;
+          if (j < E) {
+            const double a = (j != i) ? v[u][q] * inv_n[f] : 0.0;
+            dot += a * ab[q];
+            na2 += a * a;
+            dev2 += (a - ab[q]) * (a - ab[q]);
+          }
         }
+        dot = wave_sum(dot);
+        na2 = wave_sum(na2);
+        dev2 = wave_sum(dev2);
+        const double na = sqrt(na2);
+        cos_sum += (na > 0.0 && nb > 0.0) ? dot / (na * nb) : 0.0;
+        worst = fmax(worst, sqrt(dev2));
       }
-      dot = wave_sum(dot);
-      na2 = wave_sum(na2);
-      dev2 = wave_sum(dev2);
-      const double na = sqrt(na2);
-      cos_sum += (na > 0.0 && nb > 0.0) ? dot / (na * nb) : 0.0;
-      worst = fmax(worst, sqrt(dev2));
     }
     if (lane == 0) {
       const int64_t o = static_cast<int64_t>(l) * E + i;
