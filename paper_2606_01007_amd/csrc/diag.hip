@@ -3,7 +3,7 @@
 //     P_f[l][e] = D_f[l][e] / N_{f,l}, dist[i][j] = ||P_i - P_j||_F over all layers and experts;
 //   * top-n co-activated pair sets per (family, layer) and their Jaccard overlaps per layer.
 //
-// dist_kernel: one workgroup per family pair, layers in sequence, float64.
+// dist_kernel: one workgroup per family pair, one wave per layer (wave sums only), float64.
 // top_pairs_kernel: one workgroup per (family, layer).  The segment's upper triangle is staged in
 //   LDS (130,560 B at E = 256; rows by waves, coalesced), the n-th largest positive count T is found by bisection on counts,
 //   pairs above T are kept, ties at T are kept in increasing pair order until n are chosen (a
@@ -56,27 +56,42 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* buf, uint32_t& to
 
 __global__ __launch_bounds__(kDistThreads) void dist_kernel(const uint32_t* __restrict__ D, int F, int L, int E, int k,
                                                             double* __restrict__ dist) {
-  __shared__ unsigned long long red[kDistThreads / 64];
   __shared__ double dred[kDistThreads / 64];
   const int i = blockIdx.x, j = blockIdx.y;
-  const int e = threadIdx.x;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   double acc = 0.0;
-  for (int l = 0; l < L; ++l) {
-    const unsigned long long di = (e < E) ? D[(static_cast<int64_t>(i) * L + l) * E + e] : 0u;
-    const unsigned long long dj = (e < E) ? D[(static_cast<int64_t>(j) * L + l) * E + e] : 0u;
-    const unsigned long long si = block_sum_u64(di, red);
-    const unsigned long long sj = block_sum_u64(dj, red);
+  for (int l = wave; l < L; l += nw) {  // one wave per layer, lanes over experts
+    const uint32_t* Di = D + (static_cast<int64_t>(i) * L + l) * E;
+    const uint32_t* Dj = D + (static_cast<int64_t>(j) * L + l) * E;
+    uint32_t di[4], dj[4];
+    unsigned long long si = 0, sj = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = lane + 64 * q;
+      di[q] = e < E ? Di[e] : 0u;
+      dj[q] = e < E ? Dj[e] : 0u;
+      si += di[q];
+      sj += dj[q];
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      si += __shfl_xor(si, o, 64);
+      sj += __shfl_xor(sj, o, 64);
+    }
     // P = D / N with N = sum_e D / k, i.e. P = k * D / sum_e D (0 for an empty family)
-    const double pi = si ? static_cast<double>(di) / (static_cast<double>(si) / k) : 0.0;
-    const double pj = sj ? static_cast<double>(dj) / (static_cast<double>(sj) / k) : 0.0;
-    acc += (pi - pj) * (pi - pj);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const double pi = si ? static_cast<double>(di[q]) / (static_cast<double>(si) / k) : 0.0;
+      const double pj = sj ? static_cast<double>(dj[q]) / (static_cast<double>(sj) / k) : 0.0;
+      acc += (pi - pj) * (pi - pj);
+    }
   }
   acc = wave_sum_d(acc);
-  if ((threadIdx.x & 63) == 0) dred[threadIdx.x >> 6] = acc;
+  if (lane == 0) dred[wave] = acc;
   __syncthreads();
   if (threadIdx.x == 0) {
     double s = 0.0;
-    for (int w = 0; w < kDistThreads / 64; ++w) s += dred[w];
+    for (int w = 0; w < nw; ++w) s += dred[w];
     dist[static_cast<int64_t>(i) * F + j] = sqrt(s);
   }
 }
