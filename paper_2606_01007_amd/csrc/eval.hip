@@ -141,9 +141,13 @@ __global__ __launch_bounds__(256) void ev_flags(EvArgs a) {
       any = true;
     }
     if (any) {
+      // every placement marks the same few experts: set a bit only when a device-scope read does
+      // not show it yet (a stale read costs one extra atomic, never a missing bit)
       const int e = static_cast<int>(pe % a.E);
       const int l = static_cast<int>((pe / a.E) % a.L);
-      atomicOr(&a.ws.flagbits[l * 8 + (e >> 5)], 1u << (e & 31));
+      uint32_t* w = &a.ws.flagbits[l * 8 + (e >> 5)];
+      const uint32_t bit = 1u << (e & 31);
+      if (!(__hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit)) atomicOr(w, bit);
     }
   }
   if (err) atomicOr(a.d_err, err);
@@ -187,32 +191,56 @@ __global__ __launch_bounds__(256) void ev_repinfo(EvArgs a) {
   if (nrep == 0) return;
   const int G = a.G;
   const int64_t* ref = a.load_ref + (static_cast<int64_t>(p) * a.L + l) * G;
+  // this placement's snapshot loads in registers (all loads in flight at once)
+  int64_t rf[TACG_MAX_GPUS];
+#pragma unroll
+  for (int m = 0; m < TACG_MAX_GPUS; ++m) rf[m] = m < G ? ref[m] : 0;
+  // the candidate sets of the replicated experts, gathered before they are used
+  uint32_t cands[TACG_MAX_REPLICATED];
+#pragma unroll
+  for (int r = 0; r < TACG_MAX_REPLICATED; ++r) {
+    uint32_t cand = 0;
+    if (r < nrep) {
+      const int e = a.ws.rep_list[l * TACG_MAX_REPLICATED + r];
+      const int64_t pe = (static_cast<int64_t>(p) * a.L + l) * a.E + e;
+      const uint8_t g0 = a.primary[pe];
+      if (g0 < G) cand |= 1u << g0;
+      for (int q = 0; q < a.R; ++q) {
+        const uint8_t g = a.secondary[pe * a.R + q];
+        if (g < G) cand |= 1u << g;
+      }
+    }
+    cands[r] = cand;
+  }
   // eq. feasible-set with the mean load of eq. mean-load, exact in 128-bit integers
   uint32_t feas = (G == 32) ? 0xffffffffu : ((1u << G) - 1u);
   if (a.theta_den != 0) {
     __int128 total = 0;
-    for (int m = 0; m < G; ++m) total += ref[m];
+#pragma unroll
+    for (int m = 0; m < TACG_MAX_GPUS; ++m) total += rf[m];
     const __int128 rhs = static_cast<__int128>(a.theta_den + a.theta_num) * total;
     feas = 0;
-    for (int m = 0; m < G; ++m)
-      if (static_cast<__int128>(a.theta_den) * G * ref[m] <= rhs) feas |= 1u << m;
+#pragma unroll
+    for (int m = 0; m < TACG_MAX_GPUS; ++m)
+      if (m < G && static_cast<__int128>(a.theta_den) * G * rf[m] <= rhs) feas |= 1u << m;
   }
-  for (int r = 0; r < nrep; ++r) {
-    const int e = a.ws.rep_list[l * TACG_MAX_REPLICATED + r];
-    const int64_t pe = (static_cast<int64_t>(p) * a.L + l) * a.E + e;
-    uint32_t cand = 0;
-    const uint8_t g0 = a.primary[pe];
-    if (g0 < G) cand |= 1u << g0;
-    for (int q = 0; q < a.R; ++q) {
-      const uint8_t g = a.secondary[pe * a.R + q];
-      if (g < G) cand |= 1u << g;
-    }
+#pragma unroll
+  for (int r = 0; r < TACG_MAX_REPLICATED; ++r) {
+    if (r >= nrep) break;
+    uint32_t cand = cands[r];
     if (cand == 0) cand = 1u;  // invalid table (already flagged): keep the choice in range
     uint32_t fc = cand & feas;
     if (fc == 0) fc = cand;
+    // least-loaded feasible candidate, ties to the lowest GPU
     int best = -1;
-    for (int m = 0; m < G; ++m)
-      if (((fc >> m) & 1u) && (best < 0 || ref[m] < ref[best])) best = m;
+    int64_t bestv = 0;
+#pragma unroll
+    for (int m = 0; m < TACG_MAX_GPUS; ++m) {
+      if (((fc >> m) & 1u) && (best < 0 || rf[m] < bestv)) {
+        best = m;
+        bestv = rf[m];
+      }
+    }
     // bit 31: the expert has a single candidate in this placement (it is served by its primary and
     // belongs to the GPUs the token reaches before any multi-candidate slot is resolved)
     const uint32_t single = (__popc(cand) == 1) ? 0x80000000u : 0u;
