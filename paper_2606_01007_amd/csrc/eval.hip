@@ -325,17 +325,16 @@ struct Scorer {
     const uint32_t repmask = info & ((1u << IL::kMaskBits) - 1u);
     if (!repmask) return;
     const uint32_t hshift = 8u * ((info >> IL::kHomeShift) & 31u);  // 8 * band position of the anchor
+    // a scalar loop over the set bits of the (wave-uniform) mask: the replicated slots only
     int nth = 0;
-#pragma unroll
-    for (int s = 0; s < K; ++s) {
-      if (!((repmask >> s) & 1u)) continue;
+    for (uint32_t rem = repmask; rem != 0u; rem &= rem - 1u, ++nth) {
+      const int s = __builtin_ctz(rem);
       uint32_t r;
       if (nth < IL::kRepSlots) {
         r = (info >> (IL::kRepShift + 4 * nth)) & 15u;
       } else {
         r = rep_of[__builtin_amdgcn_ubfe(ids[s >> 2], 8 * (s & 3), 8)];
       }
-      ++nth;
       const uint2* rp = rinfo + r * PW + lane * PPL;
       uint2 ri[PPL];
 #pragma unroll
