@@ -287,6 +287,7 @@ struct Scorer {
   using IL = InfoLayout<K>;
 
   const char* tbl_lane;   // LDS table base + this lane's column offset
+  uint32_t row_bytes;     // PW * 4, held in a VGPR
   const uint2* rinfo;     // [MAX_REP][PW]
   uint32_t* rcnt;         // [G][PW / 2]
   const uint8_t* rep_of;  // [E]
@@ -300,7 +301,9 @@ struct Scorer {
 #pragma unroll
     for (int s = 0; s < K; ++s) {
       const uint32_t id = __builtin_amdgcn_ubfe(ids[s >> 2], 8 * (s & 3), 8);
-      const char* base = tbl_lane + (id << kRowShift);
+      // row stride in an opaque VGPR: one scalar extract and one v_mad_u32_u24 per slot (left to
+      // itself the compiler moves the shift into two scalar instructions for half of the slots)
+      const char* base = tbl_lane + __umul24(id, row_bytes);
       if constexpr (PPL == 2) {
         const uint2 v = *reinterpret_cast<const uint2*>(base);
         m[0] |= v.x;
@@ -412,6 +415,7 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
   const int16_t* trace_l = a.trace + static_cast<int64_t>(l) * a.N * K;
   S sc;
   sc.tbl_lane = reinterpret_cast<const char*>(tbl) + lane * PPL * 4;
+  asm volatile("v_mov_b32 %0, %1" : "=v"(sc.row_bytes) : "i"(S::PW * 4));
   sc.rinfo = rinfo;
   sc.rcnt = rcnt;
   sc.rep_of = rep_of;
