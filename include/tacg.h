@@ -160,6 +160,7 @@ int tacg_placement_load(const uint32_t* D, int32_t n_fam, int32_t n_layers, int3
  * Tables: uint8 primary[P][L][E]; uint8 secondary[P][L][E][R] or NULL with n_sec = 0; int64
  * load_ref[P][L][G] (required when n_sec > 0; see tacg_placement_load).  Host arrays home_start_host
  * and home_size_host [F] must satisfy home_size >= 1 and home_start + home_size <= G.
+ * theta_num and theta_den lie in 0 .. 2^20 (theta_num is not read when theta_den == 0).
  * Data errors: TACG_ERR_ID_RANGE / _DUP (trace), TACG_ERR_TABLE, TACG_ERR_LIMIT.
  * workspace: tacg_eval_workspace_bytes(...) bytes.  flags: must be 0.
  */
@@ -210,7 +211,7 @@ int tacg_eval_trace_stats(const int16_t* trace, int64_t n_tokens, int32_t n_laye
  * state_in_or_null: float64 [P][L][G] initial loads (NULL = zero); state_out_or_null: the loads
  * after the last token (may be the same buffer as state_in, so that a trace can be scored in token
  * chunks: the costs and loads of the chunks add up to those of the whole trace when every chunk keeps
- * each family's anchor phase).  0 <= rho < 1.  Tables and outputs as in tacg_eval_placements; no
+ * each family's anchor phase).  0 <= rho < 1.  theta, tables and outputs as in tacg_eval_placements; no
  * workspace and no limit on the number of replicated experts.  One wave scans 64 placements of one
  * layer, so the time grows with N and the parallelism is P * L lanes.
  * Data errors: TACG_ERR_ID_RANGE / _DUP (the token-layer is not served and does not update the

@@ -228,7 +228,8 @@ int tacg_eval_online(const int16_t* trace, int64_t n_tokens, int32_t n_layers, i
     return TACG_E_INVAL;
   if (n_sec > 0 && secondary_or_null == nullptr) return TACG_E_INVAL;
   if (!(rho >= 0.0 && rho < 1.0)) return TACG_E_INVAL;
-  if (theta_num < 0 || theta_den < 0 || theta_num > (1 << 20) || theta_den > (1 << 20)) return TACG_E_INVAL;
+  if (theta_num < 0 || theta_den < 0 || (theta_den > 0 && theta_num > (1 << 20)) || theta_den > (1 << 20))
+    return TACG_E_INVAL;
   if (home_start_host == nullptr || home_size_host == nullptr) return TACG_E_INVAL;
   for (int f = 0; f < n_fam; ++f) {
     if (home_size_host[f] < 1 || home_start_host[f] < 0 || home_start_host[f] + home_size_host[f] > n_gpus)

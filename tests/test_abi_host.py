@@ -123,6 +123,8 @@ def test_eval_argument_errors(L):
     assert call(hs_=np.array([0, 3], dtype=np.int32)) == tacg.E_INVAL     # band past G
     assert call(flags=1) == tacg.E_INVAL
     assert call(tn=-1) == tacg.E_INVAL
+    assert call(tn=(1 << 20) + 1) == tacg.E_INVAL
+    assert call(td=(1 << 20) + 1) == tacg.E_INVAL
     assert call(wsb=1) == tacg.E_INVAL
     assert call(off_=np.array([0, 60, 90], dtype=np.int64)) == tacg.E_INVAL
 
@@ -174,6 +176,8 @@ def test_eval_online_argument_errors(L):
     assert call(hs_=np.array([0, 3], dtype=np.int32)) == tacg.E_INVAL
     assert call(flags=1) == tacg.E_INVAL
     assert call(td=-1) == tacg.E_INVAL
+    assert call(tn=(1 << 20) + 1) == tacg.E_INVAL
+    assert call(td=(1 << 20) + 1) == tacg.E_INVAL
     assert call(ch=None) == tacg.E_INVAL
     assert call(off_=np.array([0, 60, 90], dtype=np.int64)) == tacg.E_INVAL
 
