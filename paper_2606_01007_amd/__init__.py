@@ -6,7 +6,7 @@ PyTorch supplies device memory and the current HIP stream; every step runs in th
 kernels.  There is no fallback: if the library or the GPU is missing, the calls raise.
 
     D, C, err = coact_build(trace, fam_off, n_experts)
-    pref, a_tilde, a_hat, err = reweight(D, C, top_k, alpha=0.25, tau=1.0, eps=1e-8)
+    pref, a_tilde, a_hat = reweight(D, C, top_k, alpha=0.25, tau=1.0, eps=1e-8)
     load_ref = placement_load(D, primary, n_gpus)
     out = eval_placements(trace, fam_off, n_experts, home_start, home_size, n_gpus, primary,
                           secondary, load_ref, theta=(3, 20))
@@ -97,6 +97,22 @@ def _dptr(t: Optional[torch.Tensor]):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _arg(t: Optional[torch.Tensor], name: str, dtype: torch.dtype, shape) -> Optional[ctypes.c_void_p]:
+    """Device pointer of `t` after checking the element type and shape the C ABI assumes (a kernel
+    would otherwise read or write past a smaller buffer)."""
+    if t is None:
+        return None
+    if t.dtype != dtype or tuple(t.shape) != tuple(int(x) for x in shape):
+        raise ValueError(f"{name}: expected {dtype} {tuple(int(x) for x in shape)}, got {t.dtype} {tuple(t.shape)}")
+    return _dptr(t)
+
+
+def _trace_dims(trace: torch.Tensor):
+    if trace.dtype != torch.int16 or trace.dim() != 3:
+        raise ValueError(f"trace: expected int16 [L][N][k], got {trace.dtype} {tuple(trace.shape)}")
+    return trace.shape
+
+
 def _stream(stream=None):
     s = stream if stream is not None else torch.cuda.current_stream()
     return ctypes.c_void_p(s.cuda_stream)
@@ -132,7 +148,7 @@ def coact_build(trace: torch.Tensor, fam_off, n_experts: int, D: Optional[torch.
                 C: Optional[torch.Tensor] = None, accumulate: bool = False, ws: Optional[torch.Tensor] = None,
                 err: Optional[torch.Tensor] = None, stream=None):
     """Counts D [F][L][E] and C [F][L][E][E] (uint32 bits in int32 tensors) and the d_err tensor."""
-    L_, N, k = trace.shape
+    L_, N, k = _trace_dims(trace)
     off = _host_i64(fam_off)
     F = off.size - 1
     dev = trace.device
@@ -145,8 +161,11 @@ def coact_build(trace: torch.Tensor, fam_off, n_experts: int, D: Optional[torch.
         ws = workspace(need, dev)
     if err is None:
         err = _err_tensor(dev)
-    st = lib().tacg_coact_build(_dptr(trace), N, L_, k, n_experts, _hptr(off), F, _dptr(D), _dptr(C),
-                                ACCUMULATE if accumulate else 0, _dptr(err), _dptr(ws), ws.numel(), _stream(stream))
+    st = lib().tacg_coact_build(_dptr(trace), N, L_, k, n_experts, _hptr(off), F,
+                                _arg(D, "D", torch.int32, (F, L_, n_experts)),
+                                _arg(C, "C", torch.int32, (F, L_, n_experts, n_experts)),
+                                ACCUMULATE if accumulate else 0, _arg(err, "err", torch.int32, (1,)),
+                                _dptr(ws), ws.numel(), _stream(stream))
     _check("tacg_coact_build", st)
     return D, C, err
 
@@ -162,7 +181,8 @@ def reweight(D: torch.Tensor, C: torch.Tensor, top_k: int, alpha: float = 0.25, 
     need = lib().tacg_reweight_workspace_bytes(F, L_, E)
     if ws is None or ws.numel() < need:
         ws = workspace(need, dev)
-    st = lib().tacg_reweight(_dptr(D), _dptr(C), F, L_, E, top_k, float(alpha), float(tau), float(eps),
+    st = lib().tacg_reweight(_arg(D, "D", torch.int32, (F, L_, E)), _arg(C, "C", torch.int32, (F, L_, E, E)), F, L_,
+                             E, top_k, float(alpha), float(tau), float(eps),
                              _dptr(pref), _dptr(at), _dptr(ah), _dptr(ws), ws.numel(), _stream(stream))
     _check("tacg_reweight", st)
     return pref, at, ah
@@ -176,8 +196,9 @@ def placement_load(D: torch.Tensor, primary: torch.Tensor, n_gpus: int, err: Opt
     out = torch.empty((P, L_, n_gpus), dtype=torch.int64, device=D.device)
     if err is None:
         err = _err_tensor(D.device)
-    st = lib().tacg_placement_load(_dptr(D), F, L_, E, _dptr(primary), P, n_gpus, _dptr(out), _dptr(err),
-                                   _stream(stream))
+    st = lib().tacg_placement_load(_arg(D, "D", torch.int32, (F, L_, E)), F, L_, E,
+                                   _arg(primary, "primary", torch.uint8, (P, L_, E)), P, n_gpus, _dptr(out),
+                                   _arg(err, "err", torch.int32, (1,)), _stream(stream))
     _check("tacg_placement_load", st)
     return out
 
@@ -188,7 +209,7 @@ def eval_placements(trace: torch.Tensor, fam_off, n_experts: int, home_start, ho
                     ws: Optional[torch.Tensor] = None, err: Optional[torch.Tensor] = None, out: Optional[dict] = None,
                     stream=None) -> dict:
     """dict(cost_home [P] int64, cost_span [P] int64, load [P][L][G] (uint32 bits), cost_home_fam, err)."""
-    L_, N, k = trace.shape
+    L_, N, k = _trace_dims(trace)
     off = _host_i64(fam_off)
     F = off.size - 1
     hs, hz = _host_i32(home_start), _host_i32(home_size)
@@ -207,10 +228,14 @@ def eval_placements(trace: torch.Tensor, fam_off, n_experts: int, home_start, ho
         err = _err_tensor(dev)
     tn, td = theta if theta is not None else (0, 0)
     st = lib().tacg_eval_placements(
-        _dptr(trace), N, L_, k, n_experts, _hptr(off), F, _hptr(hs), _hptr(hz), n_gpus, P, _dptr(primary),
-        _dptr(secondary) if R > 0 else None, R, _dptr(load_ref) if R > 0 else None, int(tn), int(td),
-        _dptr(out["cost_home"]), _dptr(out["cost_span"]), _dptr(out["load"]), _dptr(out["cost_home_fam"]), 0,
-        _dptr(err), _dptr(ws), ws.numel(), _stream(stream))
+        _dptr(trace), N, L_, k, n_experts, _hptr(off), F, _hptr(hs), _hptr(hz), n_gpus, P,
+        _arg(primary, "primary", torch.uint8, (P, L_, n_experts)),
+        _arg(secondary, "secondary", torch.uint8, (P, L_, n_experts, R)) if R > 0 else None, R,
+        _arg(load_ref, "load_ref", torch.int64, (P, L_, n_gpus)) if R > 0 else None, int(tn), int(td),
+        _arg(out["cost_home"], "cost_home", torch.int64, (P,)), _arg(out["cost_span"], "cost_span", torch.int64, (P,)),
+        _arg(out["load"], "load", torch.int32, (P, L_, n_gpus)),
+        _arg(out["cost_home_fam"], "cost_home_fam", torch.int64, (P, F)), 0,
+        _arg(err, "err", torch.int32, (1,)), _dptr(ws), ws.numel(), _stream(stream))
     _check("tacg_eval_placements", st)
     out["err"] = err
     return out
@@ -222,7 +247,7 @@ def eval_trace_stats(trace: torch.Tensor, fam_off, n_experts: int, home_start, h
                      err: Optional[torch.Tensor] = None, stream=None) -> dict:
     """Snapshot scoring plus the per-token statistics of App. C (tacg_eval_trace_stats).
     dict(cost_home, cost_span, load, span_fam, cross_fam, home_mass_fam ([P][F] int64), err)."""
-    L_, N, k = trace.shape
+    L_, N, k = _trace_dims(trace)
     off = _host_i64(fam_off)
     F = off.size - 1
     hs, hz = _host_i32(home_start), _host_i32(home_size)
@@ -242,10 +267,13 @@ def eval_trace_stats(trace: torch.Tensor, fam_off, n_experts: int, home_start, h
         err = _err_tensor(dev)
     tn, td = theta if theta is not None else (0, 0)
     st = lib().tacg_eval_trace_stats(
-        _dptr(trace), N, L_, k, n_experts, _hptr(off), F, _hptr(hs), _hptr(hz), n_gpus, P, _dptr(primary),
-        _dptr(secondary) if R > 0 else None, R, _dptr(load_ref) if R > 0 else None, int(tn), int(td),
+        _dptr(trace), N, L_, k, n_experts, _hptr(off), F, _hptr(hs), _hptr(hz), n_gpus, P,
+        _arg(primary, "primary", torch.uint8, (P, L_, n_experts)),
+        _arg(secondary, "secondary", torch.uint8, (P, L_, n_experts, R)) if R > 0 else None, R,
+        _arg(load_ref, "load_ref", torch.int64, (P, L_, n_gpus)) if R > 0 else None, int(tn), int(td),
         _dptr(out["cost_home"]), _dptr(out["cost_span"]), _dptr(out["load"]), _dptr(out["span_fam"]),
-        _dptr(out["cross_fam"]), _dptr(out["home_mass_fam"]), 0, _dptr(err), _dptr(ws), ws.numel(), _stream(stream))
+        _dptr(out["cross_fam"]), _dptr(out["home_mass_fam"]), 0, _arg(err, "err", torch.int32, (1,)), _dptr(ws),
+        ws.numel(), _stream(stream))
     _check("tacg_eval_trace_stats", st)
     out["err"] = err
     return out
@@ -257,7 +285,7 @@ def eval_online(trace: torch.Tensor, fam_off, n_experts: int, home_start, home_s
                 err: Optional[torch.Tensor] = None, out: Optional[dict] = None, stream=None) -> dict:
     """Scoring with decayed per-GPU loads (tacg_eval_online).  state: float64 [P][L][G] initial loads
     or None (zero).  dict(cost_home, cost_span, load, cost_home_fam, state (final loads), err)."""
-    L_, N, k = trace.shape
+    L_, N, k = _trace_dims(trace)
     off = _host_i64(fam_off)
     F = off.size - 1
     hs, hz = _host_i32(home_start), _host_i32(home_size)
@@ -276,10 +304,15 @@ def eval_online(trace: torch.Tensor, fam_off, n_experts: int, home_start, home_s
         err = _err_tensor(dev)
     tn, td = theta if theta is not None else (0, 0)
     st = lib().tacg_eval_online(
-        _dptr(trace), N, L_, k, n_experts, _hptr(off), F, _hptr(hs), _hptr(hz), n_gpus, P, _dptr(primary),
-        _dptr(secondary) if R > 0 else None, R, float(rho), int(tn), int(td), _dptr(state), _dptr(out.get("state")),
-        _dptr(out["cost_home"]), _dptr(out["cost_span"]), _dptr(out["load"]), _dptr(out["cost_home_fam"]), 0,
-        _dptr(err), _stream(stream))
+        _dptr(trace), N, L_, k, n_experts, _hptr(off), F, _hptr(hs), _hptr(hz), n_gpus, P,
+        _arg(primary, "primary", torch.uint8, (P, L_, n_experts)),
+        _arg(secondary, "secondary", torch.uint8, (P, L_, n_experts, R)) if R > 0 else None, R, float(rho),
+        int(tn), int(td), _dptr(state),
+        _arg(out.get("state"), "state", torch.float64, (P, L_, n_gpus)),
+        _arg(out["cost_home"], "cost_home", torch.int64, (P,)), _arg(out["cost_span"], "cost_span", torch.int64, (P,)),
+        _arg(out["load"], "load", torch.int32, (P, L_, n_gpus)),
+        _arg(out["cost_home_fam"], "cost_home_fam", torch.int64, (P, F)), 0,
+        _arg(err, "err", torch.int32, (1,)), _stream(stream))
     _check("tacg_eval_online", st)
     out["err"] = err
     return out
@@ -289,7 +322,8 @@ def activation_distance(D: torch.Tensor, top_k: int, stream=None) -> torch.Tenso
     """float64 [F][F] Frobenius distances of the families' expert-activation distributions."""
     F, L_, E = D.shape
     out = torch.empty((F, F), dtype=torch.float64, device=D.device)
-    st = lib().tacg_activation_distance(_dptr(D), F, L_, E, top_k, _dptr(out), _stream(stream))
+    st = lib().tacg_activation_distance(_arg(D, "D", torch.int32, (F, L_, E)), F, L_, E, top_k, _dptr(out),
+                                        _stream(stream))
     _check("tacg_activation_distance", st)
     return out
 
@@ -299,7 +333,8 @@ def pair_jaccard(C: torch.Tensor, top_n: int = 64, stream=None):
     F, L_, E, _ = C.shape
     pairs = torch.empty((F, L_, top_n), dtype=torch.int32, device=C.device)
     jac = torch.empty((L_, F, F), dtype=torch.float64, device=C.device)
-    st = lib().tacg_pair_jaccard(_dptr(C), F, L_, E, top_n, _dptr(pairs), _dptr(jac), _stream(stream))
+    st = lib().tacg_pair_jaccard(_arg(C, "C", torch.int32, (F, L_, E, E)), F, L_, E, top_n, _dptr(pairs), _dptr(jac),
+                                 _stream(stream))
     _check("tacg_pair_jaccard", st)
     return pairs, jac
 
@@ -310,7 +345,8 @@ def gesr_scores(D: torch.Tensor, C: torch.Tensor, top_k: int, stream=None):
     cent = torch.empty((L_, E), dtype=torch.float64, device=D.device)
     cons = torch.empty_like(cent)
     spec = torch.empty_like(cent)
-    st = lib().tacg_gesr_scores(_dptr(D), _dptr(C), F, L_, E, top_k, _dptr(cent), _dptr(cons), _dptr(spec),
+    st = lib().tacg_gesr_scores(_arg(D, "D", torch.int32, (F, L_, E)), _arg(C, "C", torch.int32, (F, L_, E, E)),
+                                F, L_, E, top_k, _dptr(cent), _dptr(cons), _dptr(spec),
                                 _stream(stream))
     _check("tacg_gesr_scores", st)
     return cent, cons, spec
@@ -324,7 +360,9 @@ def group_objective(a_tilde: torch.Tensor, primary: torch.Tensor, n_gpus: int, e
     out = torch.empty((P, L_), dtype=torch.float64, device=a_tilde.device)
     if err is None:
         err = _err_tensor(a_tilde.device)
-    st = lib().tacg_group_objective(_dptr(a_tilde), L_, E, _dptr(primary), P, n_gpus, _dptr(out), _dptr(err),
+    st = lib().tacg_group_objective(_arg(a_tilde, "a_tilde", torch.float32, (L_, E, E)), L_, E,
+                                    _arg(primary, "primary", torch.uint8, (P, L_, E)), P, n_gpus, _dptr(out),
+                                    _arg(err, "err", torch.int32, (1,)),
                                     _stream(stream))
     _check("tacg_group_objective", st)
     return out
@@ -336,6 +374,7 @@ def jain_index(load: torch.Tensor, per_layer: bool = False, stream=None):
     shape = (P, L_) if per_layer else (P,)
     j = torch.empty(shape, dtype=torch.float32, device=load.device)
     v = torch.empty(shape, dtype=torch.float32, device=load.device)
-    st = lib().tacg_jain(_dptr(load), P, L_, G, 1 if per_layer else 0, _dptr(j), _dptr(v), _stream(stream))
+    st = lib().tacg_jain(_arg(load, "load", torch.int32, (P, L_, G)), P, L_, G, 1 if per_layer else 0, _dptr(j),
+                         _dptr(v), _stream(stream))
     _check("tacg_jain", st)
     return j, v

@@ -223,3 +223,38 @@ def test_binding_refuses_host_tensors():
         tacg.coact_build(tr, [0, 4], 8, D=torch.zeros((1, 1, 8), dtype=torch.int32),
                          C=torch.zeros((1, 1, 8, 8), dtype=torch.int32), ws=torch.zeros(1 << 12, dtype=torch.uint8),
                          err=torch.zeros(1, dtype=torch.int32))
+
+
+def test_binding_checks_element_types_and_shapes():
+    """A tensor of another element type or shape than the C ABI assumes is refused before any call
+    (a kernel would otherwise read or write past a smaller buffer).  Without a GPU the public calls
+    stop at the first tensor argument (host tensors are refused too), so the later arguments' check is
+    exercised through the helper that every call uses."""
+    import torch
+    if not os.path.exists(tacg.LIB_PATH):
+        pytest.skip("libtacg.so not built")
+    ws = torch.zeros(1 << 12, dtype=torch.uint8)
+    err = torch.zeros(1, dtype=torch.int32)
+    with pytest.raises(ValueError, match="trace"):
+        tacg.coact_build(torch.zeros((1, 4, 2), dtype=torch.int32), [0, 4], 8, ws=ws, err=err)
+    with pytest.raises(ValueError, match="trace"):
+        tacg.coact_build(torch.zeros((4, 2), dtype=torch.int16), [0, 4], 8, ws=ws, err=err)
+    with pytest.raises(ValueError, match="trace"):
+        tacg.eval_placements(torch.zeros((1, 4, 2), dtype=torch.int64), [0, 4], 8, [0], [1], 1,
+                             torch.zeros((1, 1, 8), dtype=torch.uint8))
+    with pytest.raises(ValueError, match="load: expected torch.int32"):
+        tacg.jain_index(torch.zeros((2, 1, 4), dtype=torch.int64))
+    with pytest.raises(ValueError, match="a_tilde: expected torch.float32"):
+        tacg.group_objective(torch.zeros((1, 8, 8), dtype=torch.float64), torch.zeros((2, 1, 8), dtype=torch.uint8), 4,
+                             err=err)
+    with pytest.raises(ValueError, match="D: expected"):
+        tacg.placement_load(torch.zeros((1, 1, 8), dtype=torch.int16), torch.zeros((2, 1, 8), dtype=torch.uint8), 4,
+                            err=err)
+    # the helper: element type, then shape, then device
+    with pytest.raises(ValueError, match=r"D: expected torch.int32 \(1, 1, 8\), got torch.int16"):
+        tacg._arg(torch.zeros((1, 1, 8), dtype=torch.int16), "D", torch.int32, (1, 1, 8))
+    with pytest.raises(ValueError, match=r"primary: expected torch.uint8 \(2, 1, 8\), got torch.uint8 \(2, 1, 9\)"):
+        tacg._arg(torch.zeros((2, 1, 9), dtype=torch.uint8), "primary", torch.uint8, (2, 1, 8))
+    with pytest.raises(ValueError, match="device tensor"):
+        tacg._arg(torch.zeros((2, 1, 8), dtype=torch.uint8), "primary", torch.uint8, (2, 1, 8))
+    assert tacg._arg(None, "secondary", torch.uint8, (1,)) is None
