@@ -30,8 +30,11 @@ namespace {
 
 constexpr int kMainThreads = 1024;
 constexpr int kMaxPieces = 160;
-constexpr uint32_t kXcds = 8;
-constexpr int64_t kTargetWorkgroups = 4096;  // XCDs of an MI355X; workgroups are dealt to them round-robin
+constexpr uint32_t kXcds = 8;  // XCDs of an MI355X; workgroups are dealt to them round-robin
+// About 32 workgroups of ev_main per CU: short enough that the last round leaves little idle time
+// when the families' ragged last pieces make the workgroups uneven (measured 2 % faster than 4096
+// on a Dirichlet family mix), long enough to amortise the table set-up and the flushes.
+constexpr int64_t kTargetWorkgroups = 8192;
 constexpr uint8_t kNone = 0xFF;
 
 struct EvWs {
@@ -845,7 +848,7 @@ int launch_eval(const int16_t* trace, int64_t N, int32_t L, int32_t K, int32_t E
   }
   // pieces: split every family's tokens into chunks sized for about kTargetWorkgroups workgroups of
   // ev_main (at least 4096 tokens; at most 2^26 so that the per-lane 32-bit cost accumulators cannot
-  // overflow).  Fewer, longer workgroups amortise the table set-up and the per-workgroup flushes.
+  // overflow).
   const int64_t n_pblocks = (E > 64 || stats != nullptr) ? (P + 127) / 128 : (P + 255) / 256;
   int64_t chunk = (N * n_pblocks * L + kTargetWorkgroups - 1) / kTargetWorkgroups;
   chunk = std::min<int64_t>(int64_t(1) << 26, std::max<int64_t>(4096, chunk));
