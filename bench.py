@@ -180,10 +180,12 @@ def main():
     calib_dst = calib_src.clone()
     del calib_src, calib_dst
 
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+    # one set of stage events per timed step, read after the closing synchronize: no host sync
+    # inside the timed region
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(max(1, args.steps))]
     reduced = bool(args.tokens or args.layers)
 
-    def step(timed):
+    def step(timed, ev=evs[0]):
         if timed:
             ev[0].record()
         tacg.coact_build(w.trace_group, w.fam_off_group, E, D=D, C=C, ws=ws_c, err=err)
@@ -208,12 +210,12 @@ def main():
     stage = np.zeros((args.steps, 4))
     t_start = time.perf_counter()
     for s in range(args.steps):
-        step(True)
-        torch.cuda.synchronize()
-        for i in range(4):
-            stage[s, i] = ev[i].elapsed_time(ev[i + 1]) * 1e-3
+        step(True, evs[s])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
+    for s in range(args.steps):
+        for i in range(4):
+            stage[s, i] = evs[s][i].elapsed_time(evs[s][i + 1]) * 1e-3
     assert int(err.item()) == 0, f"device data error bits {int(err.item()):#x}"
 
     t_coact, t_rw, t_eval, t_jain = stage.mean(axis=0)
