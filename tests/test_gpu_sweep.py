@@ -62,7 +62,7 @@ def _draw(seed):
     return dict(E=E, k=k, L=L, counts=counts, G=G, cap=cap, P=P, R=R, n_rep=n_rep, theta=theta, rho=rho)
 
 
-@pytest.mark.parametrize("seed", range(64))
+@pytest.mark.parametrize("seed", range(256))
 def test_random_shape_sweep(seed):
     c = _draw(seed)
     E, k, L, G, P, R = c["E"], c["k"], c["L"], c["G"], c["P"], c["R"]
