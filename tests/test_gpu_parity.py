@@ -66,6 +66,10 @@ def _rand_trace(L, N, k, E, seed, device="cuda"):
     (32, 12, 2, [1500, 500], 10),
     (100, 6, 2, [2500, 1700], 11),
     (129, 7, 3, [999, 3001], 12),
+    # several histogram workgroups (one per 32768 token-layers) whose ranges cross segment boundaries
+    (256, 8, 3, [30000, 17, 25000], 13),
+    (128, 8, 2, [40000, 33000], 14),
+    (60, 4, 2, [50000, 20000, 1], 15),
 ])
 def test_coact_parity(E, k, L, counts, seed):
     _say(f"coact E={E} k={k} L={L} counts={counts}")
