@@ -14,6 +14,8 @@
  *     TACG_E_DEVICE.  Data errors found on the device are OR-ed into *d_err (a uint32 the caller
  *     zeroes before the call); the outputs of a call that set any d_err bit are unspecified.
  *   - Layouts are C-contiguous (last index fastest).
+ *   - Alignment: the trace pointer is 16-byte aligned and every workspace 256-byte aligned
+ *     (TACG_E_INVAL otherwise); other buffers need only their element alignment.
  *
  * Routing traces: int16 trace[L][N][k] -- for each MoE layer l and token t, the k expert ids the
  * router selected (slot 0 = highest router score).  Tokens are grouped by task family: family f owns
