@@ -18,6 +18,11 @@ Paper passages followed (Sec. = section of the paper):
   scoring              Sec. 3.4 eqs. mean-load, feasible-set (+ fallback), candidate-set; App. C
                        per-token dispatch sets; App. H "Comm"
   Jain, MaxVio         App. H eqs. jain, maxvio;  Comm. Red.: App. H eq. comm-red
+  decayed-load scoring Sec. 3.4 eq. load-update (the sequential form of the serving rule)
+  grouping objective   Sec. 3.3 eq. grouping-objective
+  GESR scores          Sec. 3.4 eq. generic-score (Cent, Cons, Spec)
+  trace statistics     App. C statistics (i)-(iii) per family (score(..., stats=True))
+  diagnostics          App. H auxiliary motivation metrics (activation distance, top-pair Jaccard)
 
 Readings where the paper is silent:
   * u = D / (N_f k) (sums to 1 over experts); A = C / N_f off the diagonal, A(e, e) = 0;
