@@ -3,7 +3,8 @@ counts, in the launch configuration the benchmark times; the decayed-load scorin
 sample of the serving trace, its first 2^19 tokens).
 
 The oracle computes sampled outputs one by one (a few family/layer segments of the counts, the
-reweighted graph of sampled layers, a few scored placements over the whole trace); every other
+reweighted graph of sampled layers, a few scored placements over the whole trace, with the per-token
+statistics of App. C); every other
 output is checked through properties that hold at any size (symmetry, diagonal, row sums and
 totals of the counts; per-layer load totals and cost bounds of the scores).
 """
@@ -103,15 +104,25 @@ def test_full_size(name):
         assert bool((ch >= 0).all()) and bool((ch <= Ns * L * min(k, G - 1)).all())
         assert bool((cs >= 0).all()) and bool((cs <= Ns * L * (min(k, G) - 1)).all())
         assert torch.equal(out["cost_home_fam"].sum(dim=1), ch)
+        # the per-token statistics of App. C (their own kernel variant) in the same launch configuration
+        st = tacg.eval_trace_stats(w.trace_serve, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, prim,
+                                   sec, ref_g, theta=(3, 20))
+        torch.cuda.synchronize()
+        assert int(st["err"].item()) == 0
+        for key in ("cost_home", "cost_span", "load"):
+            assert torch.equal(st[key], out[key]), key
+        assert torch.equal(st["span_fam"].sum(dim=1), cs)
         for p in sorted({0, P // 2, P - 1}):
             _say(f"[{name}] oracle scoring placement {p} of {P} (G={G})")
             ro = oracle.score(ts, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, ps["primary"],
-                              ps["secondary"], ref_o, (3, 20), p_range=(p, p + 1))
+                              ps["secondary"], ref_o, (3, 20), p_range=(p, p + 1), stats=True)
             assert ro["err"] == 0
             assert int(ch[p]) == int(ro["cost_home"][p])
             assert int(cs[p]) == int(ro["cost_span"][p])
             np.testing.assert_array_equal(load[p].cpu().numpy(), ro["load"][p])
             np.testing.assert_array_equal(out["cost_home_fam"][p].cpu().numpy(), ro["cost_home_fam"][p])
+            for key in ("span_fam", "cross_fam", "home_mass_fam"):
+                np.testing.assert_array_equal(st[key][p].cpu().numpy(), ro[key][p], err_msg=key)
             jo, vo = oracle.jain(ro["load"][p:p + 1])
             np.testing.assert_allclose(float(jn[p]), jo[0], rtol=1e-5)
             np.testing.assert_allclose(float(mv[p]), vo[0], rtol=1e-5, atol=1e-30)
