@@ -3,8 +3,9 @@ counts, in the launch configuration the benchmark times; the decayed-load scorin
 sample of the serving trace, its first 2^19 tokens).
 
 The oracle computes sampled outputs one by one (a few family/layer segments of the counts, the
-reweighted graph of sampled layers, a few scored placements over the whole trace, with the per-token
-statistics of App. C); every other
+reweighted graph, GESR scores, top pairs, Jaccard overlaps and grouping objective of sampled layers,
+the activation distance, a few scored placements over the whole trace with the per-token statistics
+of App. C); every other
 output is checked through properties that hold at any size (symmetry, diagonal, row sums and
 totals of the counts; per-layer load totals and cost bounds of the scores).
 """
@@ -65,6 +66,7 @@ def test_full_size(name):
 
     # ---- reweighting: sampled layers against the oracle (counts recomputed by the oracle) ----
     pref, at, _ = tacg.reweight(D, C, k)
+    per_layer = {}
     for l in [0, L - 1]:
         Dol = np.zeros((F, 1, E), np.int64)
         Col = np.zeros((F, 1, E, E), np.int64)
@@ -73,8 +75,34 @@ def test_full_size(name):
         po, ato, _ = oracle.reweight(Dol, Col, k)
         np.testing.assert_allclose(pref[l].cpu().double().numpy(), po[0], rtol=1e-5, atol=1e-30)
         np.testing.assert_allclose(at[l].cpu().double().numpy(), ato[0], rtol=1e-5, atol=1e-30)
-    del tg
+        per_layer[l] = (Dol, Col, ato[0])
     _say(f"[{name}] reweight ok")
+
+    # ---- the auxiliary calls of the benchmark on the full counts: sampled layers against the oracle ----
+    cent, cons, spec = tacg.gesr_scores(D, C, k)
+    pairs, jac = tacg.pair_jaccard(C, 64)
+    dist = tacg.activation_distance(D, k)
+    for l, (Dol, Col, ato_l) in per_layer.items():
+        co, so, sp = oracle.gesr_scores(Dol, Col, k)
+        np.testing.assert_allclose(cent[l].cpu().numpy(), co[0], rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(cons[l].cpu().numpy(), so[0], rtol=1e-12, atol=1e-15)
+        np.testing.assert_allclose(spec[l].cpu().numpy(), sp[0], rtol=1e-12, atol=1e-15)
+        np.testing.assert_array_equal(pairs[:, l].cpu().numpy(), oracle.top_pairs(Col, 64)[:, 0])
+        np.testing.assert_array_equal(jac[l].cpu().numpy(), oracle.pair_jaccard(Col, 64)[0])
+    Do_all, _, _ = oracle.coact(tg, w.fam_off_group, E)   # every layer's D for the distance (C dropped)
+    np.testing.assert_allclose(dist.cpu().numpy(), oracle.activation_distance(Do_all, k), rtol=1e-12, atol=1e-15)
+    del tg, Do_all
+    ps = w.placement_sets[0]
+    prim0 = torch.as_tensor(ps["primary"]).cuda()
+    obj = tacg.group_objective(at, prim0, ps["n_gpus"])           # all placements x layers, as benchmarked
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(obj).all()) and bool((obj >= 0).all())
+    for l, (_, _, ato_l) in per_layer.items():                    # the oracle's graph on both sides
+        a32 = ato_l.astype(np.float32)[None]
+        got = tacg.group_objective(torch.as_tensor(a32).cuda(), prim0[:, l:l + 1].contiguous(), ps["n_gpus"])
+        ref = oracle.grouping_objective(a32.astype(np.float64), ps["primary"][:, l:l + 1], ps["n_gpus"])
+        np.testing.assert_allclose(got.cpu().numpy(), ref, rtol=1e-12, atol=1e-300)
+    _say(f"[{name}] auxiliary calls ok")
 
     # ---- placement scoring at full size: every placement set of the preset ----
     ts = w.trace_serve.cpu().numpy()
