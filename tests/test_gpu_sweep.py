@@ -1,13 +1,15 @@
-"""A seeded sweep over random small shapes: every entry point of the hot path (co-activation counts,
+"""A seeded sweep over random shapes: every entry point of the hot path (co-activation counts,
 reweighting, snapshot scoring with its App. C statistics, decayed-load scoring, Jain / MaxVio and the
 grouping objective) against the oracle on the same inputs.
 
 The shapes are drawn to reach the kernels' branches in combination: expert counts on both sides of
 the 64 / 128 launch thresholds, every top-k width from 1 to 16 (packed ids of one to four words, the
-matrix-core path at E <= 64 and k >= 5), one to five families with empty ones, 1 to 32 GPUs with
-narrow and wide bands, zero to four secondaries with up to 16 replicated experts, the guard on and
-off, and decay factors 0, 0.5 and 0.995.  Counts, costs, loads and the final float64 loads are
-compared exactly; float outputs within the tolerances of the other parity tests.
+matrix-core path at E <= 64 and k >= 5), one to five small families with empty ones, 1 to 32 GPUs
+with narrow and wide bands, zero to four secondaries with up to 16 replicated experts, the guard on
+and off, and decay factors 0, 0.5 and 0.995.  A large-shape variant draws up to eight families of up
+to 60,000 tokens (some nearly empty), so that several co-activation workgroups meet at segment
+boundaries and the scoring kernel runs many pieces.  Counts, costs, loads and the final float64
+loads are compared exactly; float outputs within the tolerances of the other parity tests.
 """
 import sys
 
@@ -62,9 +64,36 @@ def _draw(seed):
     return dict(E=E, k=k, L=L, counts=counts, G=G, cap=cap, P=P, R=R, n_rep=n_rep, theta=theta, rho=rho)
 
 
+def _draw_large(seed):
+    """Larger families (5,000 to 60,000 tokens, some nearly empty): several co-activation workgroups
+    per segment boundary and many scoring pieces."""
+    rng = np.random.default_rng(9000 + seed)
+    E = int(rng.choice([60, 64, 100, 128, 129, 200, 256]))
+    k = int(rng.integers(2, min(E, 16) + 1))
+    L = int(rng.integers(1, 4))
+    F = int(rng.integers(1, 9))
+    counts = [int(rng.integers(5000, 60000)) if rng.random() > 0.15 else int(rng.integers(0, 50)) for _ in range(F)]
+    G = int(rng.choice([2, 4, 8, 16, 32]))
+    cap = -(-E // G) + int(rng.integers(0, 3))
+    P = int(rng.integers(1, 300))
+    R = int(rng.integers(0, min(4, G - 1) + 1))
+    n_rep = min(int(rng.integers(1, 17)), E) if R > 0 else 0
+    theta = [(3, 20), (0, 0), (1, 10)][int(rng.integers(0, 3))]
+    rho = [0.0, 0.5, 0.995][int(rng.integers(0, 3))]
+    return dict(E=E, k=k, L=L, counts=counts, G=G, cap=cap, P=P, R=R, n_rep=n_rep, theta=theta, rho=rho)
+
+
 @pytest.mark.parametrize("seed", range(256))
 def test_random_shape_sweep(seed):
-    c = _draw(seed)
+    _check(_draw(seed), seed)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_large_shape_sweep(seed):
+    _check(_draw_large(seed), seed)
+
+
+def _check(c, seed):
     E, k, L, G, P, R = c["E"], c["k"], c["L"], c["G"], c["P"], c["R"]
     _say(f"sweep seed={seed} {c}")
     off = synth.fam_offsets(c["counts"])
