@@ -135,7 +135,7 @@ struct CodeRegs {
 };
 
 // grid (ceil(P / 64), L), 64 threads; NG = 8 or 32 >= G GPUs in registers.
-template <int K, int NG>
+template <int K, int NG, int MC>
 __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
   extern __shared__ __align__(16) uint32_t lds[];
   constexpr int KB = (K + 3) / 4;  // dwords of 8-bit ids per token-layer
@@ -316,13 +316,13 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
               cm = candidate_mask(a, live, base + e, unused);
             }
           }
-          // the candidates in increasing GPU order (at most kMaxCand) and their loads
+          // the candidates in increasing GPU order (at most MC: 4 when R <= 3, else 5) and their loads
           const int ncand = __popc(cm);
-          uint32_t g[kMaxCand];
-          double v[kMaxCand];
+          uint32_t g[MC];
+          double v[MC];
           uint32_t rest = cm;
 #pragma unroll
-          for (int i = 0; i < kMaxCand; ++i) {
+          for (int i = 0; i < MC; ++i) {
             g[i] = min(find_first_bit(rest), static_cast<uint32_t>(NG - 1));  // ffbl(0) = ~0: unused
             rest &= rest - 1u;
             v[i] = Lc[((g[i] >> 1) * kLanes + lane) * 2 + (g[i] & 1u)];
@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
           if (guard) {
             uint32_t feas = 0;
 #pragma unroll
-            for (int i = 0; i < kMaxCand; ++i) feas |= (i < ncand && gden * v[i] <= rhs) ? (1u << g[i]) : 0u;
+            for (int i = 0; i < MC; ++i) feas |= (i < ncand && gden * v[i] <= rhs) ? (1u << g[i]) : 0u;
             fc = feas ? feas : cm;
           }
           // least loaded in fc; candidates come in increasing GPU order, so a strict < keeps the
@@ -340,7 +340,7 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
           double best = 0.0;
           bool found = false;
 #pragma unroll
-          for (int i = 0; i < kMaxCand; ++i) {
+          for (int i = 0; i < MC; ++i) {
             const bool in = i < ncand && ((fc >> g[i]) & 1u);
             const bool better = in && (!found || v[i] < best);
             best = better ? v[i] : best;
@@ -392,20 +392,26 @@ __global__ __launch_bounds__(kLanes) void on_main(OnArgs a) {
   if (err) atomicOr(a.d_err, err);
 }
 
-template <int K, int NG>
+template <int K, int NG, int MC>
 void launch_on_t(const OnArgs& a, hipStream_t stream) {
   // candidate rows, counters, expert counts, then the larger of the code bytes and the loads
   const size_t lds = (static_cast<size_t>(kRows) * kLanes + 32 * kLanes + TACG_MAX_EXPERTS + 8) * sizeof(uint32_t) +
                      std::max(static_cast<size_t>(TACG_MAX_EXPERTS) * kLanes, static_cast<size_t>(NG) * kLanes * 8);
-  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&on_main<K, NG>),
+  (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&on_main<K, NG, MC>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-  hipLaunchKernelGGL((on_main<K, NG>), dim3((a.P + kLanes - 1) / kLanes, a.L), dim3(kLanes), lds, stream, a);
+  hipLaunchKernelGGL((on_main<K, NG, MC>), dim3((a.P + kLanes - 1) / kLanes, a.L), dim3(kLanes), lds, stream, a);
 }
 
 template <int K>
 void launch_on(const OnArgs& a, hipStream_t stream) {
-  if (a.G <= 8) launch_on_t<K, 8>(a, stream);
-  else launch_on_t<K, 32>(a, stream);
+  // a slot has at most R + 1 candidates: four-entry candidate lists when R <= 3
+  if (a.G <= 8) {
+    if (a.R <= 3) launch_on_t<K, 8, 4>(a, stream);
+    else launch_on_t<K, 8, kMaxCand>(a, stream);
+  } else {
+    if (a.R <= 3) launch_on_t<K, 32, 4>(a, stream);
+    else launch_on_t<K, 32, kMaxCand>(a, stream);
+  }
 }
 
 }  // namespace
