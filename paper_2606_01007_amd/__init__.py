@@ -130,6 +130,23 @@ def _hptr(a: np.ndarray):
     return a.ctypes.data_as(ctypes.c_void_p)
 
 
+def _fam_off(fam_off) -> np.ndarray:
+    """fam_off as int64 [F+1] with F >= 1 (the C ABI reads F + 1 entries)."""
+    off = _host_i64(fam_off)
+    if off.ndim != 1 or off.size < 2:
+        raise ValueError(f"fam_off: expected a 1-D sequence of F + 1 >= 2 offsets, got shape {off.shape}")
+    return off
+
+
+def _bands(home_start, home_size, F: int):
+    """home_start, home_size as int32 [F] each (the C ABI reads F entries of both)."""
+    hs, hz = _host_i32(home_start), _host_i32(home_size)
+    if hs.ndim != 1 or hz.ndim != 1 or hs.size != F or hz.size != F:
+        raise ValueError(f"home_start / home_size: expected {F} entries each (one per family), "
+                         f"got shapes {hs.shape} and {hz.shape}")
+    return hs, hz
+
+
 def as_u32(t: torch.Tensor) -> torch.Tensor:
     """int64 values of a uint32 buffer held in an int32 tensor."""
     return t.to(torch.int64) & 0xFFFFFFFF
@@ -149,7 +166,7 @@ def coact_build(trace: torch.Tensor, fam_off, n_experts: int, D: Optional[torch.
                 err: Optional[torch.Tensor] = None, stream=None):
     """Counts D [F][L][E] and C [F][L][E][E] (uint32 bits in int32 tensors) and the d_err tensor."""
     L_, N, k = _trace_dims(trace)
-    off = _host_i64(fam_off)
+    off = _fam_off(fam_off)
     F = off.size - 1
     dev = trace.device
     if D is None:
@@ -210,9 +227,9 @@ def eval_placements(trace: torch.Tensor, fam_off, n_experts: int, home_start, ho
                     stream=None) -> dict:
     """dict(cost_home [P] int64, cost_span [P] int64, load [P][L][G] (uint32 bits), cost_home_fam, err)."""
     L_, N, k = _trace_dims(trace)
-    off = _host_i64(fam_off)
+    off = _fam_off(fam_off)
     F = off.size - 1
-    hs, hz = _host_i32(home_start), _host_i32(home_size)
+    hs, hz = _bands(home_start, home_size, F)
     P = primary.shape[0]
     dev = trace.device
     R = 0 if secondary is None else int(secondary.shape[-1])
@@ -248,9 +265,9 @@ def eval_trace_stats(trace: torch.Tensor, fam_off, n_experts: int, home_start, h
     """Snapshot scoring plus the per-token statistics of App. C (tacg_eval_trace_stats).
     dict(cost_home, cost_span, load, span_fam, cross_fam, home_mass_fam ([P][F] int64), err)."""
     L_, N, k = _trace_dims(trace)
-    off = _host_i64(fam_off)
+    off = _fam_off(fam_off)
     F = off.size - 1
-    hs, hz = _host_i32(home_start), _host_i32(home_size)
+    hs, hz = _bands(home_start, home_size, F)
     P = primary.shape[0]
     dev = trace.device
     R = 0 if secondary is None else int(secondary.shape[-1])
@@ -286,9 +303,9 @@ def eval_online(trace: torch.Tensor, fam_off, n_experts: int, home_start, home_s
     """Scoring with decayed per-GPU loads (tacg_eval_online).  state: float64 [P][L][G] initial loads
     or None (zero).  dict(cost_home, cost_span, load, cost_home_fam, state (final loads), err)."""
     L_, N, k = _trace_dims(trace)
-    off = _host_i64(fam_off)
+    off = _fam_off(fam_off)
     F = off.size - 1
-    hs, hz = _host_i32(home_start), _host_i32(home_size)
+    hs, hz = _bands(home_start, home_size, F)
     P = primary.shape[0]
     dev = trace.device
     R = 0 if secondary is None else int(secondary.shape[-1])

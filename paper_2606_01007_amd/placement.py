@@ -26,22 +26,9 @@ from __future__ import annotations
 
 import numpy as np
 
+from .synth import capacities  # noqa: F401  (per-GPU capacities, shared with the input generator)
+
 NONE = 0xFF
-
-
-def capacities(E: int, G: int, cap: int) -> np.ndarray:
-    """Per-GPU capacities: `cap` each, the last GPUs trimmed so that they sum to E."""
-    c = np.full(G, cap, dtype=np.int64)
-    excess = int(c.sum()) - E
-    if excess < 0:
-        raise ValueError(f"{G} GPUs x capacity {cap} cannot hold {E} experts")
-    g = G - 1
-    while excess > 0:
-        d = min(excess, int(c[g]))
-        c[g] -= d
-        excess -= d
-        g -= 1
-    return c
 
 
 def _kmeans(X: np.ndarray, k: int, rng: np.random.Generator, n_init: int, iters: int) -> np.ndarray:

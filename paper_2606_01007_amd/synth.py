@@ -227,7 +227,7 @@ def capacities(E: int, G: int, cap: int) -> np.ndarray:
     c = np.full(G, cap, dtype=np.int64)
     excess = int(c.sum()) - E
     if excess < 0:
-        raise ValueError("capacity too small")
+        raise ValueError(f"{G} GPUs x capacity {cap} cannot hold {E} experts")
     g = G - 1
     while excess > 0:
         d = min(excess, int(c[g]))

@@ -258,3 +258,27 @@ def test_binding_checks_element_types_and_shapes():
     with pytest.raises(ValueError, match="device tensor"):
         tacg._arg(torch.zeros((2, 1, 8), dtype=torch.uint8), "primary", torch.uint8, (2, 1, 8))
     assert tacg._arg(None, "secondary", torch.uint8, (1,)) is None
+
+
+def test_binding_checks_family_offsets_and_bands():
+    """The C ABI reads F + 1 family offsets and F entries of each home-band array; a shorter or
+    multi-dimensional list is refused with ValueError before any call (it would otherwise be an
+    out-of-bounds host read)."""
+    import torch
+    if not os.path.exists(tacg.LIB_PATH):
+        pytest.skip("libtacg.so not built")
+    tr = torch.zeros((1, 4, 2), dtype=torch.int16)
+    prim = torch.zeros((1, 1, 8), dtype=torch.uint8)
+    for call in (tacg.eval_placements, tacg.eval_trace_stats, tacg.eval_online):
+        with pytest.raises(ValueError, match="home_start / home_size"):
+            call(tr, [0, 2, 4], 8, [0], [1, 1], 2, prim)            # F = 2, one start
+        with pytest.raises(ValueError, match="home_start / home_size"):
+            call(tr, [0, 2, 4], 8, [0, 1], [1], 2, prim)            # F = 2, one size
+        with pytest.raises(ValueError, match="home_start / home_size"):
+            call(tr, [0, 4], 8, [[0]], [[1]], 2, prim)              # not 1-D
+        with pytest.raises(ValueError, match="fam_off"):
+            call(tr, [4], 8, [], [], 2, prim)                       # no family
+        with pytest.raises(ValueError, match="fam_off"):
+            call(tr, [[0, 4]], 8, [0], [1], 2, prim)                # not 1-D
+    with pytest.raises(ValueError, match="fam_off"):
+        tacg.coact_build(tr, [4], 8)

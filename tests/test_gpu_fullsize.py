@@ -2,12 +2,13 @@
 counts, in the launch configuration the benchmark times; the decayed-load scoring on the benchmark's
 sample of the serving trace, its first 2^19 tokens).
 
-The oracle computes sampled outputs one by one (a few family/layer segments of the counts, the
-reweighted graph, GESR scores, top pairs, Jaccard overlaps and grouping objective of sampled layers,
-the activation distance, a few scored placements over the whole trace with the per-token statistics
-of App. C); every other
-output is checked through properties that hold at any size (symmetry, diagonal, row sums and
-totals of the counts; per-layer load totals and cost bounds of the scores).
+The oracle computes the whole of D and C (every family/layer segment, compared bit for bit) and the
+activation distance; the reweighted graph, GESR scores, top pairs, Jaccard overlaps and grouping
+objective of sampled layers; and fifteen scored placements per placement set over the whole trace
+(first and last lanes of placement blocks, interior lanes, every placement position within a lane,
+several blocks), with the per-token statistics of App. C.  Every other output is checked through
+properties that hold at any size (symmetry, diagonal, row sums and totals of the counts; per-layer
+load totals and cost bounds of the scores).
 """
 import sys
 
@@ -38,6 +39,18 @@ def _u32(t):
     return tacg.as_u32(t)
 
 
+def sampled_placements(P: int, n_experts: int):
+    """Placements compared with the oracle one by one.  The scoring kernel gives each lane two
+    placements (four when E <= 64) and each workgroup 64 lanes' worth, so the sample covers the first
+    and last lanes of blocks, interior lanes, every position within a lane's group and several blocks."""
+    ppl = 4 if n_experts <= 64 else 2
+    pb = 64 * ppl
+    want = {0, 1, 2, 3, 37, 2 * 37 + 1, pb - 2, pb - 1, pb, pb + 1, P // 2 + 5, P // 2 + 70, (3 * P) // 4 + 43,
+            P - 2, P - 1}
+    return sorted(p for p in want if 0 <= p < P)
+
+
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", ["deepseek16b", "qwen15", "qwen3_30b", "deepseek_v3"])
 def test_full_size(name):
     cfg = synth.CONFIGS[name]
@@ -46,7 +59,7 @@ def test_full_size(name):
     E, k, L, F = cfg.E, cfg.k, cfg.L, cfg.F
     Ng = w.trace_group.shape[1]
 
-    # ---- co-activation counts: properties on every segment, oracle on sampled segments ----
+    # ---- co-activation counts: properties and the oracle on every segment ----
     D, C, err = tacg.coact_build(w.trace_group, w.fam_off_group, E)
     torch.cuda.synchronize()
     assert int(err.item()) == 0
@@ -57,21 +70,21 @@ def test_full_size(name):
     assert torch.equal(Cl.sum(dim=3) - Dl, (k - 1) * Dl)
     assert torch.equal(Dl.sum(dim=2), (nf[:, None] * k).expand(F, L))
     tg = w.trace_group.cpu().numpy()
-    for f, l in [(0, 0), (F // 2, L // 2), (F - 1, L - 1)]:
-        Do, Co, e = oracle.coact_segment(tg, w.fam_off_group, E, f, l)
-        assert e == 0
-        np.testing.assert_array_equal(Dl[f, l].cpu().numpy(), Do)
-        np.testing.assert_array_equal(Cl[f, l].cpu().numpy(), Co)
+    _say(f"[{name}] oracle counts of the whole grouping trace")
+    Do_all, Co_all, e = oracle.coact(tg, w.fam_off_group, E)
+    assert e == 0
+    # every (family, layer) segment of D and C, bit for bit
+    np.testing.assert_array_equal(Dl.cpu().numpy(), Do_all)
+    np.testing.assert_array_equal(Cl.cpu().numpy(), Co_all)
+    del Dl, Cl
     _say(f"[{name}] counts ok")
 
-    # ---- reweighting: sampled layers against the oracle (counts recomputed by the oracle) ----
+    # ---- reweighting: sampled layers against the oracle (on the oracle's counts) ----
     pref, at, _ = tacg.reweight(D, C, k)
     per_layer = {}
     for l in [0, L - 1]:
-        Dol = np.zeros((F, 1, E), np.int64)
-        Col = np.zeros((F, 1, E, E), np.int64)
-        for f in range(F):
-            Dol[f, 0], Col[f, 0], _ = oracle.coact_segment(tg, w.fam_off_group, E, f, l)
+        Dol = np.ascontiguousarray(Do_all[:, l:l + 1])
+        Col = np.ascontiguousarray(Co_all[:, l:l + 1])
         po, ato, _ = oracle.reweight(Dol, Col, k)
         np.testing.assert_allclose(pref[l].cpu().double().numpy(), po[0], rtol=1e-5, atol=1e-30)
         np.testing.assert_allclose(at[l].cpu().double().numpy(), ato[0], rtol=1e-5, atol=1e-30)
@@ -89,9 +102,8 @@ def test_full_size(name):
         np.testing.assert_allclose(spec[l].cpu().numpy(), sp[0], rtol=1e-12, atol=1e-15)
         np.testing.assert_array_equal(pairs[:, l].cpu().numpy(), oracle.top_pairs(Col, 64)[:, 0])
         np.testing.assert_array_equal(jac[l].cpu().numpy(), oracle.pair_jaccard(Col, 64)[0])
-    Do_all, _, _ = oracle.coact(tg, w.fam_off_group, E)   # every layer's D for the distance (C dropped)
     np.testing.assert_allclose(dist.cpu().numpy(), oracle.activation_distance(Do_all, k), rtol=1e-12, atol=1e-15)
-    del tg, Do_all
+    del tg, Do_all, Co_all
     ps = w.placement_sets[0]
     prim0 = torch.as_tensor(ps["primary"]).cuda()
     obj = tacg.group_objective(at, prim0, ps["n_gpus"])           # all placements x layers, as benchmarked
@@ -140,7 +152,7 @@ def test_full_size(name):
         for key in ("cost_home", "cost_span", "load"):
             assert torch.equal(st[key], out[key]), key
         assert torch.equal(st["span_fam"].sum(dim=1), cs)
-        for p in sorted({0, P // 2, P - 1}):
+        for p in sampled_placements(P, n_experts=E):
             _say(f"[{name}] oracle scoring placement {p} of {P} (G={G})")
             ro = oracle.score(ts, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, ps["primary"],
                               ps["secondary"], ref_o, (3, 20), p_range=(p, p + 1), stats=True)
@@ -171,7 +183,7 @@ def test_full_size(name):
     assert bool((load.sum(dim=2) == n * k).all())
     assert torch.equal(on["cost_home_fam"].sum(dim=1), on["cost_home"])
     tsn = np.ascontiguousarray(ts[:, :n])
-    for p in sorted({0, P // 2, P - 1}):
+    for p in sampled_placements(P, n_experts=E):
         _say(f"[{name}] oracle decayed-load scoring placement {p} of {P} (G={G}, {n} tokens)")
         ro = oracle.score_online(tsn, off, E, ps["home_start"], ps["home_size"], G, ps["primary"], ps["secondary"],
                                  rho=0.995, theta=(3, 20), p_range=(p, p + 1))
