@@ -40,6 +40,7 @@ extern "C" {
 #define TACG_E_INVAL (-1)
 #define TACG_E_UNSUPPORTED (-2)
 #define TACG_E_DEVICE (-3)
+#define TACG_E_SCRATCH (-4) /* tacg_eval_placements_noalloc: workspace need > TACG_NOALLOC_SCRATCH_BYTES */
 
 /* device-side data-error bits OR-ed into *d_err */
 #define TACG_ERR_ID_RANGE 0x1u /* an expert id < 0 or >= E                               */
@@ -58,6 +59,7 @@ extern "C" {
 #define TACG_MAX_SECONDARY 4
 #define TACG_MAX_REPLICATED 16
 #define TACG_MAX_TOP_PAIRS 4096
+#define TACG_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20) /* device scratch of the no-allocation entry point */
 
 /*
  * Dispatch and co-activation counts per task family and layer (Sec. 3.3, "Scoring task-family
@@ -177,6 +179,32 @@ int tacg_eval_placements(const int16_t* trace, int64_t n_tokens, int32_t n_layer
 
 size_t tacg_eval_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t n_experts, int32_t n_gpus,
                                  int32_t n_place, int32_t n_fam);
+
+/*
+ * tacg_eval_placements without a workspace argument, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).  Arguments,
+ * outputs, data errors and results are those of tacg_eval_placements; inputs and outputs are still
+ * the caller's buffers.
+ * Scratch: the library's own file-scope device array of TACG_NOALLOC_SCRATCH_BYTES (32 MiB), one copy
+ * per GPU, held from the first call on that GPU until the process ends.  Its device address is looked
+ * up on the first call on each GPU (the caller's current device, which must be the stream's device).
+ * The call allocates nothing (no hipMalloc, hipFree or allocating library routine); it clears the
+ * scratch itself on the stream before use, so the contents a previous call left do not matter.
+ * Every call on one GPU shares that GPU's scratch: calls that overlap on one GPU (concurrent streams,
+ * or threads enqueueing at once) race on it and give unspecified results; serialise them.
+ * Returns TACG_E_SCRATCH, before anything is enqueued, when tacg_eval_workspace_bytes(...) of the
+ * arguments exceeds TACG_NOALLOC_SCRATCH_BYTES (at E = 256, L = 58, G = 32 and F = 16 it holds up to
+ * 2115 placements); TACG_E_DEVICE if the scratch address cannot be obtained.
+ */
+int tacg_eval_placements_noalloc(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
+                                 int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam,
+                                 const int32_t* home_start_host, const int32_t* home_size_host,
+                                 int32_t n_gpus, int32_t n_place, const uint8_t* primary,
+                                 const uint8_t* secondary_or_null, int32_t n_sec,
+                                 const int64_t* load_ref_or_null, int32_t theta_num, int32_t theta_den,
+                                 uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
+                                 uint64_t* cost_home_fam_or_null, uint32_t flags, uint32_t* d_err,
+                                 void* hip_stream);
 
 /*
  * The per-token trace statistics of App. C, per placement and family f, on top of everything

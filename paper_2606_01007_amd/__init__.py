@@ -28,7 +28,8 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libtacg.so")
 
-OK, E_INVAL, E_UNSUPPORTED, E_DEVICE = 0, -1, -2, -3
+OK, E_INVAL, E_UNSUPPORTED, E_DEVICE, E_SCRATCH = 0, -1, -2, -3, -4
+NOALLOC_SCRATCH_BYTES = 32 << 20
 ERR_ID_RANGE, ERR_ID_DUP, ERR_TABLE, ERR_LIMIT = 0x1, 0x2, 0x4, 0x8
 ACCUMULATE = 0x1
 NONE = 0xFF
@@ -62,6 +63,8 @@ def lib():
             L.tacg_placement_load.argtypes = [P, i32, i32, i32, P, i32, i32, P, P, P]
             L.tacg_eval_placements.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, P, P, i32, P, i32, i32,
                                                P, P, P, P, u32, P, P, sz, P]
+            L.tacg_eval_placements_noalloc.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, P, P, i32, P,
+                                                       i32, i32, P, P, P, P, u32, P, P]
             L.tacg_eval_trace_stats.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, i32, i32, P, P, i32, P, i32,
                                                 i32, P, P, P, P, P, P, u32, P, P, sz, P]
             L.tacg_eval_workspace_bytes.argtypes = [i64, i32, i32, i32, i32, i32]
@@ -76,7 +79,7 @@ def lib():
             L.tacg_strerror.argtypes = [ctypes.c_int]
             L.tacg_strerror.restype = ctypes.c_char_p
             for name in ("tacg_coact_build", "tacg_reweight", "tacg_placement_load", "tacg_eval_placements",
-                         "tacg_eval_trace_stats", "tacg_jain"):
+                         "tacg_eval_placements_noalloc", "tacg_eval_trace_stats", "tacg_jain"):
                 getattr(L, name).restype = ctypes.c_int
             _lib = L
     return _lib
@@ -254,6 +257,42 @@ def eval_placements(trace: torch.Tensor, fam_off, n_experts: int, home_start, ho
         _arg(out["cost_home_fam"], "cost_home_fam", torch.int64, (P, F)), 0,
         _arg(err, "err", torch.int32, (1,)), _dptr(ws), ws.numel(), _stream(stream))
     _check("tacg_eval_placements", st)
+    out["err"] = err
+    return out
+
+
+def eval_placements_noalloc(trace: torch.Tensor, fam_off, n_experts: int, home_start, home_size, n_gpus: int,
+                            primary: torch.Tensor, secondary: Optional[torch.Tensor] = None,
+                            load_ref: Optional[torch.Tensor] = None, theta=(3, 20), err: Optional[torch.Tensor] = None,
+                            out: Optional[dict] = None, stream=None) -> dict:
+    """eval_placements through tacg_eval_placements_noalloc: no workspace; the library's own device
+    scratch (NOALLOC_SCRATCH_BYTES per GPU) serves instead.  Pass `out` (and `err`) to make the call
+    itself allocate nothing.  Same dict as eval_placements."""
+    L_, N, k = _trace_dims(trace)
+    off = _fam_off(fam_off)
+    F = off.size - 1
+    hs, hz = _bands(home_start, home_size, F)
+    P = primary.shape[0]
+    dev = trace.device
+    R = 0 if secondary is None else int(secondary.shape[-1])
+    if out is None:
+        out = dict(cost_home=torch.empty(P, dtype=torch.int64, device=dev),
+                   cost_span=torch.empty(P, dtype=torch.int64, device=dev),
+                   load=torch.empty((P, L_, n_gpus), dtype=torch.int32, device=dev),
+                   cost_home_fam=torch.empty((P, F), dtype=torch.int64, device=dev))
+    if err is None:
+        err = _err_tensor(dev)
+    tn, td = theta if theta is not None else (0, 0)
+    st = lib().tacg_eval_placements_noalloc(
+        _dptr(trace), N, L_, k, n_experts, _hptr(off), F, _hptr(hs), _hptr(hz), n_gpus, P,
+        _arg(primary, "primary", torch.uint8, (P, L_, n_experts)),
+        _arg(secondary, "secondary", torch.uint8, (P, L_, n_experts, R)) if R > 0 else None, R,
+        _arg(load_ref, "load_ref", torch.int64, (P, L_, n_gpus)) if R > 0 else None, int(tn), int(td),
+        _arg(out["cost_home"], "cost_home", torch.int64, (P,)), _arg(out["cost_span"], "cost_span", torch.int64, (P,)),
+        _arg(out["load"], "load", torch.int32, (P, L_, n_gpus)),
+        _arg(out.get("cost_home_fam"), "cost_home_fam", torch.int64, (P, F)), 0,
+        _arg(err, "err", torch.int32, (1,)), _stream(stream))
+    _check("tacg_eval_placements_noalloc", st)
     out["err"] = err
     return out
 

@@ -1,6 +1,7 @@
 // C ABI of libtacg: host-side argument validation, then enqueue on the caller's stream.
 // Argument errors return before any HIP call, so they can be exercised on a machine without a GPU.
 #include <cstdint>
+#include <mutex>
 
 #include "tacg_internal.h"
 
@@ -116,13 +117,13 @@ size_t tacg_eval_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t n_e
 
 namespace {
 
-// Checks shared by the two snapshot-scoring entry points.
-int check_eval(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
-               const int64_t* fam_off_host, int32_t n_fam, const int32_t* home_start_host,
-               const int32_t* home_size_host, int32_t n_gpus, int32_t n_place, const uint8_t* primary,
-               const uint8_t* secondary_or_null, int32_t n_sec, const int64_t* load_ref_or_null, int32_t theta_num,
-               int32_t theta_den, const uint64_t* cost_home, const uint64_t* cost_span, const uint32_t* load,
-               uint32_t flags, const uint32_t* d_err, const void* workspace, size_t workspace_bytes) {
+// Checks shared by the snapshot-scoring entry points (everything but the workspace).
+int check_eval_args(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+                    const int64_t* fam_off_host, int32_t n_fam, const int32_t* home_start_host,
+                    const int32_t* home_size_host, int32_t n_gpus, int32_t n_place, const uint8_t* primary,
+                    const uint8_t* secondary_or_null, int32_t n_sec, const int64_t* load_ref_or_null,
+                    int32_t theta_num, int32_t theta_den, const uint64_t* cost_home, const uint64_t* cost_span,
+                    const uint32_t* load, uint32_t flags, const uint32_t* d_err) {
   int rc = check_trace(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam);
   if (rc != TACG_OK) return rc;
   if (flags != 0) return TACG_E_INVAL;
@@ -138,8 +139,47 @@ int check_eval(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t
     if (home_size_host[f] < 1 || home_start_host[f] < 0 || home_start_host[f] + home_size_host[f] > n_gpus)
       return TACG_E_INVAL;
   }
+  return TACG_OK;
+}
+
+// ... plus a caller-owned workspace of tacg_eval_workspace_bytes(...) bytes, 256-byte aligned.
+int check_eval(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
+               const int64_t* fam_off_host, int32_t n_fam, const int32_t* home_start_host,
+               const int32_t* home_size_host, int32_t n_gpus, int32_t n_place, const uint8_t* primary,
+               const uint8_t* secondary_or_null, int32_t n_sec, const int64_t* load_ref_or_null, int32_t theta_num,
+               int32_t theta_den, const uint64_t* cost_home, const uint64_t* cost_span, const uint32_t* load,
+               uint32_t flags, const uint32_t* d_err, const void* workspace, size_t workspace_bytes) {
+  const int rc = check_eval_args(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, home_start_host,
+                                 home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec,
+                                 load_ref_or_null, theta_num, theta_den, cost_home, cost_span, load, flags, d_err);
+  if (rc != TACG_OK) return rc;
   const size_t need = tacg_eval_workspace_bytes(n_tokens, n_layers, n_experts, n_gpus, n_place, n_fam);
   if (workspace == nullptr || workspace_bytes < need || !aligned(workspace, 256)) return TACG_E_INVAL;
+  return TACG_OK;
+}
+
+// ---- device scratch of tacg_eval_placements_noalloc ----
+// One copy of this array lives on every GPU the library runs on, from the first use until the process
+// ends.  In host code its name is only a stand-in for the symbol: the device address of each GPU's
+// copy comes from hipGetSymbolAddress with that GPU current, and only that address is handed to
+// kernels.
+static __device__ __align__(256) unsigned char scratch[TACG_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current GPU's scratch (looked up once per device).
+int current_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TACG_E_DEVICE;
+  std::lock_guard<std::mutex> guard(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return TACG_E_DEVICE;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return TACG_OK;
 }
 
@@ -188,6 +228,29 @@ int tacg_eval_placements(const int16_t* trace, int64_t n_tokens, int32_t n_layer
                            home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec, load_ref_or_null,
                            theta_num, theta_den, cost_home, cost_span, load, cost_home_fam_or_null, nullptr, d_err,
                            workspace, as_stream(hip_stream));
+}
+
+int tacg_eval_placements_noalloc(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
+                                 int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam,
+                                 const int32_t* home_start_host, const int32_t* home_size_host, int32_t n_gpus,
+                                 int32_t n_place, const uint8_t* primary, const uint8_t* secondary_or_null,
+                                 int32_t n_sec, const int64_t* load_ref_or_null, int32_t theta_num,
+                                 int32_t theta_den, uint64_t* cost_home, uint64_t* cost_span, uint32_t* load,
+                                 uint64_t* cost_home_fam_or_null, uint32_t flags, uint32_t* d_err,
+                                 void* hip_stream) {
+  const int rc = check_eval_args(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, home_start_host,
+                                 home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec,
+                                 load_ref_or_null, theta_num, theta_den, cost_home, cost_span, load, flags, d_err);
+  if (rc != TACG_OK) return rc;
+  if (tacg_eval_workspace_bytes(n_tokens, n_layers, n_experts, n_gpus, n_place, n_fam) > TACG_NOALLOC_SCRATCH_BYTES)
+    return TACG_E_SCRATCH;
+  void* ws = nullptr;
+  const int sr = current_scratch(&ws);
+  if (sr != TACG_OK) return sr;
+  return tacg::launch_eval(trace, n_tokens, n_layers, top_k, n_experts, fam_off_host, n_fam, home_start_host,
+                           home_size_host, n_gpus, n_place, primary, secondary_or_null, n_sec, load_ref_or_null,
+                           theta_num, theta_den, cost_home, cost_span, load, cost_home_fam_or_null, nullptr, d_err,
+                           ws, as_stream(hip_stream));
 }
 
 int tacg_eval_trace_stats(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
@@ -271,6 +334,8 @@ const char* tacg_strerror(int status) {
       return "argument beyond a supported limit";
     case TACG_E_DEVICE:
       return "HIP launch failed";
+    case TACG_E_SCRATCH:
+      return "input needs more scratch than the no-allocation entry point holds (TACG_NOALLOC_SCRATCH_BYTES)";
     default:
       return "unknown status";
   }

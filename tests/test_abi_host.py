@@ -282,3 +282,34 @@ def test_binding_checks_family_offsets_and_bands():
             call(tr, [[0, 4]], 8, [0], [1], 2, prim)                # not 1-D
     with pytest.raises(ValueError, match="fam_off"):
         tacg.coact_build(tr, [4], 8)
+
+
+def _noalloc(L, **kw):
+    a = dict(trace=FAKE, N=100, Ly=2, k=2, E=8, off=np.array([0, 50, 100], dtype=np.int64), F=2,
+             hs=np.array([0, 1], dtype=np.int32), hz=np.array([1, 1], dtype=np.int32), G=2, P=4, prim=FAKE,
+             sec=None, R=0, ref=None, tn=3, td=20, ch=FAKE, cs=FAKE, load=FAKE, fam=None, flags=0, err=FAKE)
+    a.update(kw)
+    return L.tacg_eval_placements_noalloc(
+        a["trace"], a["N"], a["Ly"], a["k"], a["E"], a["off"].ctypes.data_as(ctypes.c_void_p), a["F"],
+        a["hs"].ctypes.data_as(ctypes.c_void_p), a["hz"].ctypes.data_as(ctypes.c_void_p), a["G"], a["P"],
+        a["prim"], a["sec"], a["R"], a["ref"], a["tn"], a["td"], a["ch"], a["cs"], a["load"], a["fam"], a["flags"],
+        a["err"], None)
+
+
+def test_noalloc_argument_errors_and_scratch_limit(L):
+    """The no-allocation entry point checks its arguments like tacg_eval_placements and refuses, before
+    anything is enqueued, an input whose scratch need exceeds the fixed device array."""
+    assert tacg.NOALLOC_SCRATCH_BYTES == 32 << 20
+    assert _noalloc(L, G=0) == tacg.E_INVAL
+    assert _noalloc(L, G=33) == tacg.E_UNSUPPORTED
+    assert _noalloc(L, prim=None) == tacg.E_INVAL
+    assert _noalloc(L, R=1) == tacg.E_INVAL                    # secondaries without tables
+    assert _noalloc(L, flags=1) == tacg.E_INVAL
+    assert _noalloc(L, hz=np.array([1, 2], dtype=np.int32)) == tacg.E_INVAL   # band past G
+    # 58 layers, E = 256, G = 32, 16 families: 2115 placements fit in 32 MiB, 2116 do not
+    big = dict(N=1 << 10, Ly=58, k=8, E=256, off=np.linspace(0, 1 << 10, 17).astype(np.int64), F=16,
+               hs=np.arange(16, dtype=np.int32) * 2, hz=np.full(16, 2, dtype=np.int32), G=32)
+    assert L.tacg_eval_workspace_bytes(1 << 10, 58, 256, 32, 2115, 16) <= tacg.NOALLOC_SCRATCH_BYTES
+    assert L.tacg_eval_workspace_bytes(1 << 10, 58, 256, 32, 2116, 16) > tacg.NOALLOC_SCRATCH_BYTES
+    assert _noalloc(L, P=2116, **big) == tacg.E_SCRATCH
+    assert b"no-allocation" in L.tacg_strerror(tacg.E_SCRATCH)
