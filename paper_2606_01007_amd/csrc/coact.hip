@@ -17,7 +17,7 @@
 //     workspace (slot indices are unique because both w and s grow along x), then zeroes it.
 //   * A second kernel, one workgroup per segment, sums the partial slots of the workgroups that
 //     touched the segment and writes the dense symmetric C (diagonal = D) and D.
-//   * At E <= 64 and k >= 5 the partial slots come from int8 matrix products instead
+//   * At E <= 64 and k >= 5 the partial slots come from 4-bit matrix products instead
 //     (coact_mfma.hip), with the same split of x, the same slots and the same reduction.
 #include "tacg_internal.h"
 
@@ -273,15 +273,27 @@ __global__ __launch_bounds__(kReduceThreads) void coact_reduce_kernel(CoactArgs 
   }
   const int nb = a.nbins;  // >= 1
   constexpr int kUnroll = 4 * NQ;  // about nbins / kReduceThreads loads per thread
+  // slots summed per round: about 16 loads per thread in flight (many workgroups' slots meet in one
+  // segment when each workgroup covers a short range, as on the matrix-core path)
+  constexpr int kSlots = kUnroll >= 16 ? 1 : 16 / kUnroll;
   for (int b0 = threadIdx.x; b0 < nb; b0 += kUnroll * kReduceThreads) {
     uint32_t v[kUnroll] = {};
-    for (int64_t w = w0; w <= w1; ++w) {
-      const uint32_t* src = a.partial + (w + s) * static_cast<int64_t>(nb);
-      uint32_t x[kUnroll];
+    for (int64_t w = w0; w <= w1; w += kSlots) {
+      uint32_t x[kSlots][kUnroll];
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) x[u] = __builtin_nontemporal_load(src + min(b0 + u * kReduceThreads, nb - 1));
+      for (int j = 0; j < kSlots; ++j) {
+        // slots past w1 are read clamped to w1 (in bounds) and then dropped
+        const uint32_t* src = a.partial + (min(w + j, w1) + s) * static_cast<int64_t>(nb);
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) v[u] += x[u];
+        for (int u = 0; u < kUnroll; ++u)
+          x[j][u] = __builtin_nontemporal_load(src + min(b0 + u * kReduceThreads, nb - 1));
+      }
+#pragma unroll
+      for (int j = 0; j < kSlots; ++j) {
+        const uint32_t keep = (w + j <= w1) ? ~0u : 0u;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) v[u] += x[j][u] & keep;
+      }
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {

@@ -1,25 +1,32 @@
 // Co-activation counts of small expert counts (E <= 64) on the matrix cores.
 //
 // For the tokens of one (family, layer) segment, C = R^T R where R[t][e] = 1 when token t selected
-// expert e (Sec. 3.3: C counts the tokens that chose both experts).  With E <= 64 the whole Gram
-// matrix is at most 2 x 2 blocks of 32 x 32, and the int8 MFMA v_mfma_i32_32x32x32_i8 adds the
-// products of 32 tokens per instruction; at E = 64, top-6 that is 6 matrix instructions per 64
-// token-layers instead of 15 scattered LDS increments per token-layer.  Used for k >= 5, where it
-// is faster than the histogram (coact.hip).
+// expert e (Sec. 3.3: C counts the tokens that chose both experts).  With E <= 32 NB the Gram matrix
+// has NB x NB blocks of 32 x 32 (NB = 1 or 2); v_mfma_f32_32x32x64_f8f6f4 with 4-bit (e2m1)
+// operands adds the products of 64 tokens per instruction, so 64 token-layers cost NB (NB + 1) / 2
+// matrix instructions (the blocks on and above the diagonal), whatever k is.
 //
 // Kernel design (gfx950): one wave per workgroup; W waves each take one contiguous range of the
-// flattened token-layers x = l * N + t (the same split as the histogram kernel, so the partial slots
-// and the reduction are shared).  The ids of the next four batches are in flight while one is
-// counted.  Per batch of 64 token-layers (one per lane):
-//   * every lane validates its token's ids (range, repeats) and writes a 1 byte at [id][lane] of a
-//     wave-private LDS tile [64 experts][64 tokens] (row stride 80 bytes, so that the 16-byte fragment
-//     reads of eight consecutive lanes cover all 32 banks);
-//   * for each half of the batch (32 tokens), lane l reads the 16 bytes of expert 32 i + l % 32 for
-//     tokens 16 (l / 32) .. + 15 of that half: this one fragment is both the A operand (rows of R^T)
-//     and the B operand (columns of R) of block i, since the k-th byte of a lane's A and B operands
-//     stand for the same token;
-//   * the blocks (0, 0), (0, 1) and (1, 1) accumulate in 32-bit registers ((1, 0) is the transpose);
-//   * the bytes are cleared again by the same lanes.
+// flattened token-layers x = l * N + t (the split of the histogram kernel, so the partial slots and
+// the reduction are shared).  The ids of the next four batches are in flight while one is counted.
+// Per batch of 64 token-layers (one per lane):
+//   * each lane forms its token's one-hot row in registers: a 64-bit mask of its ids (which also
+//     validates them: a repeated id leaves fewer than k bits), spread to one e2m1 nibble per expert
+//     (0x1 = 0.5, so a product is 0.25 and every float32 partial sum is exact);
+//   * the lane stores the row (16 NB bytes, token-major) into a wave-private LDS tile with 16-byte
+//     writes.  The 8-byte chunks of a row (16 experts each) sit at positions permuted by the row
+//     number (chunk c of row j at c ^ s(j)), which makes the reads below bank-conflict-free, and
+//     the lanes whose rows share banks write their 16-byte parts in different orders (part q ^ g(j)
+//     in store q), which makes the stores conflict-free; both permutations are XOR constants per
+//     lane, applied to the ids before the mask is formed, so they cost nothing per token;
+//   * ds_read_b64_tr_b4 reads 16 rows x 16 nibbles per group of 16 lanes and hands lane i the
+//     nibbles of column i: two such reads give lane l the 32 nibbles of expert 32 b + l % 32 over
+//     tokens 32 (l / 32) .. + 31 of the batch.  That fragment is both the A operand (row of R^T) and
+//     the B operand (column of R) of block b, since the j-th nibble of a lane's A and B operands
+//     stands for the same token; the product is exact whatever the hardware's k order.
+// No clearing is needed (every row is overwritten), and two tiles alternate, so a wave's writes of
+// one batch never meet its reads of the previous one.  The LDS executes one wave's instructions in
+// order, so the reads see the same wave's preceding writes without a barrier.
 // At a segment boundary the wave writes the strict upper triangle of its counts into partial slot
 // w + s (every bin, so no clearing is needed) and starts again from zero.
 #include "tacg_internal.h"
@@ -27,11 +34,13 @@
 namespace tacg {
 namespace {
 
+typedef int v2i __attribute__((ext_vector_type(2)));
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kRow = 80;                 // bytes per expert row of the tile (64 tokens + padding)
-constexpr int kTile = 64 * kRow;         // bytes of the wave's tile
+constexpr int kFmtFp4 = 4;  // operand format code of the f8f6f4 matrix instructions: e2m1
 
 struct MfmaArgs {
   const int16_t* trace;
@@ -49,44 +58,110 @@ __device__ __forceinline__ uint32_t tri_bin(uint32_t m, uint32_t n, uint32_t E) 
 }
 
 // Write the strict upper triangle of one 32 x 32 accumulator block (bi, bj).  Accumulator register r
-// of lane l holds row 8 (r / 4) + 4 (l / 32) + r % 4 and column l % 32 of the block.
-__device__ __forceinline__ void store_block(const v16i& acc, int bi, int bj, int lane, uint32_t E,
+// of lane l holds row 8 (r / 4) + 4 (l / 32) + r % 4 and column l % 32 of the block, as 0.25 x count.
+__device__ __forceinline__ void store_block(const v16f& acc, int bi, int bj, int lane, uint32_t E,
                                             uint32_t* __restrict__ dst) {
   const uint32_t n = 32u * bj + (lane & 31);
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const uint32_t m = 32u * bi + 8u * (r >> 2) + 4u * (lane >> 5) + (r & 3);
-    if (m < n && n < E) dst[tri_bin(m, n, E)] = static_cast<uint32_t>(acc[r]);
+    if (m < n && n < E) dst[tri_bin(m, n, E)] = static_cast<uint32_t>(acc[r] * 4.0f);
   }
 }
 
-// The raw ids of one token-layer (k int16 values), fetched ahead of their use.
+// The raw ids of one token-layer, fetched ahead of their use (k int16 values; dword loads for even k).
 template <int K>
 struct Raw {
-  uint16_t v[K];
+  static constexpr int kWords = (K % 2 == 0) ? K / 2 : K;
+  uint32_t w[kWords];
   __device__ __forceinline__ void fetch(const int16_t* __restrict__ p) {
+    if constexpr (K % 2 == 0) {
 #pragma unroll
-    for (int s = 0; s < K; ++s) v[s] = static_cast<uint16_t>(__builtin_nontemporal_load(p + s));
+      for (int q = 0; q < kWords; ++q) w[q] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(p) + q);
+    } else {
+#pragma unroll
+      for (int q = 0; q < kWords; ++q) w[q] = static_cast<uint16_t>(__builtin_nontemporal_load(p + q));
+    }
+  }
+  __device__ __forceinline__ uint32_t id(int s) const {  // negative ids become >= 32768 >= E
+    if constexpr (K % 2 == 0) return (s & 1) ? (w[s >> 1] >> 16) : (w[s >> 1] & 0xffffu);
+    else return w[s];
   }
 };
 
-constexpr int kDepth = 4;  // batches of ids in flight per lane
+// Eight one-hot bits -> eight nibbles of value 1 (bit n to bit 4 n).
+__device__ __forceinline__ uint32_t spread_nibbles(uint32_t x) {
+  x = (x | (x << 12)) & 0x000F000Fu;
+  x = (x | (x << 6)) & 0x03030303u;
+  x = (x | (x << 3)) & 0x11111111u;
+  return x;
+}
 
+constexpr int kDepth = 4;  // batches of ids in flight per lane (even: steps alternate the two tiles)
+
+// Add one batch's products: the blocks (bi, bj), bi <= bj, of the Gram matrix, in row order (fp4
+// operands in the low four registers of each 8-register operand).
+template <int NB>
+__device__ __forceinline__ void mfma_blocks(const v4i (&frag)[NB], v16f (&acc)[NB * (NB + 1) / 2]) {
+  v8i f[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) f[b] = v8i{frag[b].x, frag[b].y, frag[b].z, frag[b].w, 0, 0, 0, 0};
+  int b = 0;
+#pragma unroll
+  for (int bi = 0; bi < NB; ++bi) {
+#pragma unroll
+    for (int bj = bi; bj < NB; ++bj, ++b)
+      acc[b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(f[bi], f[bj], acc[b], kFmtFp4, kFmtFp4, 0, 0, 0, 0);
+  }
+}
+
+constexpr int log2i(int x) { return x <= 1 ? 0 : 1 + log2i(x / 2); }
+
+// NB = number of 32-expert blocks (1: E <= 32, 2: E <= 64).  The register budget is set for four
+// waves per SIMD (the three accumulator blocks take 48 registers).
 template <int K, int NB>
-__global__ __launch_bounds__(64) void coact_mfma_kernel(MfmaArgs a) {
-  __shared__ __align__(16) uint8_t tile[kTile];
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void coact_mfma_kernel(MfmaArgs a) {
+  static_assert(NB == 1 || NB == 2, "one or two 32-expert blocks");
+  constexpr int kRowBytes = 16 * NB;                 // 4-bit one-hot row of 32 NB experts
+  constexpr int kChunks = 2 * NB;                    // 8-byte chunks (16 experts) per row
+  constexpr int kSwShift = log2i(128 / kRowBytes);   // s(j) = (j >> kSwShift) & (kChunks - 1)
+  constexpr int kPartShift = log2i(8 / NB);          // g(j) = (j >> kPartShift) & (NB - 1)
+  constexpr int kBlocks = NB * (NB + 1) / 2;
+  constexpr int kTileBytes = 64 * kRowBytes;
+  __shared__ __align__(16) uint8_t tile[2 * kTileBytes];
   const int lane = threadIdx.x;
   const uint32_t E = static_cast<uint32_t>(a.E);
-  // clear the tile once; afterwards every batch clears the bytes it set
-  for (int i = lane * 16; i < kTile; i += 64 * 16) *reinterpret_cast<v4i*>(tile + i) = v4i{0, 0, 0, 0};
-  __syncthreads();
 
   const int64_t w = blockIdx.x;
   int64_t pos = (w * a.total) / a.W;
   const int64_t end = ((w + 1) * a.total) / a.W;
   uint32_t err = 0;
-  // this lane's fragment offsets: expert row 32 i + lane % 32, tokens 16 (lane / 32) .. + 15
-  const int frag0 = (lane & 31) * kRow + 16 * (lane >> 5);
+
+  // this lane's row (token lane of the batch): the physical chunk of logical chunk c is c ^ s(j);
+  // store q writes the row's 16-byte part q ^ g(j), so register chunk slot t holds physical chunk
+  // t ^ 2 g(j), i.e. logical chunk t ^ 2 g(j) ^ s(j): the ids are XOR-ed with that constant
+  const uint32_t sw_row = (static_cast<uint32_t>(lane) >> kSwShift) & (kChunks - 1);
+  const uint32_t part_row = (static_cast<uint32_t>(lane) >> kPartShift) & (NB - 1);
+  const uint32_t id_xor = (sw_row ^ (part_row << 1)) << 4;
+  const uint32_t row_off = static_cast<uint32_t>(lane) * kRowBytes;
+  // transposed reads: lane l = 16 g + i reads, for block b and half r, the chunk of experts
+  // 32 b + 16 (g & 1) .. + 15 of row j = 32 (g >> 1) + 16 r + i
+  uint32_t rd_off[NB][2];
+  {
+    const int g = lane >> 4, i = lane & 15;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        const uint32_t j = 32u * (g >> 1) + 16u * r + i;
+        const uint32_t c = 2u * b + (g & 1);
+        const uint32_t p = c ^ ((j >> kSwShift) & (kChunks - 1));
+        rd_off[b][r] = j * kRowBytes + 8u * p;
+      }
+    }
+  }
+  // LDS byte offset of the tile: the low 32 bits of a generic address into the LDS aperture
+  const uint32_t tile_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(tile));
 
   while (pos < end) {
     const int64_t l = pos / a.N;
@@ -94,70 +169,96 @@ __global__ __launch_bounds__(64) void coact_mfma_kernel(MfmaArgs a) {
     int f = 0;
     while (a.fam_off[f + 1] <= t0) ++f;
     const int64_t stop = min(end, l * a.N + a.fam_off[f + 1]);
-    const int64_t last = stop - 1;
-    v16i acc00 = {}, acc01 = {}, acc11 = {};
-    // ids of the next kDepth batches in flight; fetch addresses are clamped to the segment's last
-    // token-layer, so every load is in bounds and the loop is uniform
+    // this wave's part of the segment, addressed with 32-bit offsets from a uniform pointer (the
+    // host keeps every wave's range below 2^24 token-layers, for the 24-bit offset products)
+    const int16_t* __restrict__ segp = a.trace + pos * K;
+    const uint32_t n = static_cast<uint32_t>(stop - pos);
+    const uint32_t nlast = n - 1u;
+    v16f acc[kBlocks];
+#pragma unroll
+    for (int b = 0; b < kBlocks; ++b) acc[b] = v16f{};
+    // ids of the next kDepth batches in flight; fetch offsets are clamped to the last token-layer,
+    // so every load is in bounds and the loop is uniform
     Raw<K> ring[kDepth];
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) {
-      ring[d].fetch(a.trace + min(pos + 64 * d + lane, last) * K);
+      ring[d].fetch(segp + __umul24(min(static_cast<uint32_t>(64 * d + lane), nlast), static_cast<uint32_t>(K)));
       __builtin_amdgcn_sched_barrier(0);
     }
-    for (int64_t xb = pos; xb < stop; xb += 64 * kDepth) {
+    // software pipeline: the transposed reads of batch i are issued right after its rows are
+    // stored, and its matrix instructions run only after batch i + 1's rows are built, so the VALU
+    // work of the next batch covers the read latency.  Step d of the unrolled loop always uses tile
+    // d % 2 (kDepth is even), so all LDS addresses are fixed.
+    bool have = false;  // frag holds the fragments of a batch whose products are still to be added
+    v4i frag[NB];
+    for (uint32_t rb = 0; rb < n; rb += 64 * kDepth) {
 #pragma unroll
       for (int d = 0; d < kDepth; ++d) {
-        const int64_t x = xb + 64 * d + lane;
-        uint32_t ids[K];
-        bool use = false;
-        {
-          unsigned long long seen = 0;
-          bool ok = true, dup = false;
+        const uint32_t r = rb + 64u * d + lane;
+        // one-hot mask of the ids in register order (the 64-bit shift uses the low six bits of its
+        // amount); validity: every id below E, k distinct ids
+        uint64_t m = 0;
+        uint32_t idmax = 0;
 #pragma unroll
-          for (int s = 0; s < K; ++s) {
-            const uint32_t id = ring[d].v[s];  // negative ids became >= 32768 >= E
-            ok &= id < E;
-            const unsigned long long bit = 1ull << (id & 63u);
-            dup |= (seen & bit) != 0ull;
-            seen |= bit;
-            ids[s] = id;
-          }
-          if (x < stop) {
-            if (!ok) err |= TACG_ERR_ID_RANGE;
-            else if (dup) err |= TACG_ERR_ID_DUP;
-            use = ok && !dup;  // an invalid token-layer is flagged and not counted
+        for (int s = 0; s < K; ++s) {
+          const uint32_t id = ring[d].id(s);
+          idmax = max(idmax, id);
+          m |= 1ull << (id ^ id_xor);
+        }
+        const bool in_seg = r < n;
+        const bool range_bad = idmax >= E;
+        const bool dup = __builtin_popcountll(m) != K;
+        err |= (in_seg && range_bad) ? TACG_ERR_ID_RANGE : 0u;
+        err |= (in_seg && !range_bad && dup) ? TACG_ERR_ID_DUP : 0u;
+        if (!in_seg || range_bad || dup) m = 0;  // an invalid token-layer is flagged and not counted
+        ring[d].fetch(segp + __umul24(min(r + 64u * kDepth, nlast), static_cast<uint32_t>(K)));
+        const bool active = rb + 64u * d < n;  // batch-uniform
+        const uint32_t kBuf = (d & 1) * kTileBytes;
+        if (active) {
+          uint8_t* rowp = tile + kBuf + row_off;
+#pragma unroll
+          for (int q = 0; q < NB; ++q) {  // register part q (32 experts) to the row's part q ^ g(j)
+            const uint32_t src = static_cast<uint32_t>(m >> (32 * q));
+            u32x4 v;
+            v.x = spread_nibbles(src & 0xffu);
+            v.y = spread_nibbles((src >> 8) & 0xffu);
+            v.z = spread_nibbles((src >> 16) & 0xffu);
+            v.w = spread_nibbles(src >> 24);
+            *reinterpret_cast<u32x4*>(rowp + 16 * (q ^ part_row)) = v;
           }
         }
-        ring[d].fetch(a.trace + min(x + 64 * kDepth, last) * K);
-        if (xb + 64 * d < stop) {  // batch-uniform: skip the matrix work of batches past the segment end
-          if (use) {
+        if (have) mfma_blocks<NB>(frag, acc);  // the previous batch
+        have = false;
+        if (active) {
+          // the reads address the tile through raw LDS offsets the compiler cannot relate to the
+          // stores above: keep them in program order (the LDS then executes them in order)
+          __asm__ __volatile__("" ::: "memory");
 #pragma unroll
-            for (int s = 0; s < K; ++s) tile[ids[s] * kRow + lane] = 1;
+          for (int b = 0; b < NB; ++b) {
+            const v2i r0 = __builtin_amdgcn_ds_read_tr4_b64_v2i32(
+                (__attribute__((address_space(3))) v2i*)(uintptr_t)(tile_base + kBuf + rd_off[b][0]));
+            const v2i r1 = __builtin_amdgcn_ds_read_tr4_b64_v2i32(
+                (__attribute__((address_space(3))) v2i*)(uintptr_t)(tile_base + kBuf + rd_off[b][1]));
+            frag[b] = v4i{r0.x, r0.y, r1.x, r1.y};
           }
-          __syncthreads();
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {  // the two halves of 32 tokens
-            const v4i f0 = *reinterpret_cast<const v4i*>(tile + frag0 + 32 * h);
-            acc00 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f0, f0, acc00, 0, 0, 0);
-            if constexpr (NB == 2) {
-              const v4i f1 = *reinterpret_cast<const v4i*>(tile + 32 * kRow + frag0 + 32 * h);
-              acc01 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f0, f1, acc01, 0, 0, 0);
-              acc11 = __builtin_amdgcn_mfma_i32_32x32x32_i8(f1, f1, acc11, 0, 0, 0);
-            }
-          }
-          __syncthreads();
-          if (use) {
-#pragma unroll
-            for (int s = 0; s < K; ++s) tile[ids[s] * kRow + lane] = 0;
-          }
+          __asm__ __volatile__("" ::: "memory");
+          have = true;
         }
       }
     }
+    if (have) mfma_blocks<NB>(frag, acc);
     uint32_t* dst = a.partial + (w + l * a.F + f) * static_cast<int64_t>(a.nbins);
-    store_block(acc00, 0, 0, lane, E, dst);
-    if constexpr (NB == 2) {
-      store_block(acc01, 0, 1, lane, E, dst);
-      store_block(acc11, 1, 1, lane, E, dst);
+    // the bin addresses depend only on the lane: an opaque copy of E keeps the compiler from
+    // hoisting all 48 of them out of the segment loop into registers
+    uint32_t Es = E;
+    __asm__ __volatile__("" : "+s"(Es));
+    {
+      int b = 0;
+#pragma unroll
+      for (int bi = 0; bi < NB; ++bi) {
+#pragma unroll
+        for (int bj = bi; bj < NB; ++bj) store_block(acc[b++], bi, bj, lane, Es, dst);
+      }
     }
     pos = stop;
   }
@@ -173,12 +274,14 @@ void launch_k(const MfmaArgs& a, hipStream_t stream) {
 }  // namespace
 
 // The matrix path costs about the same at any k, the histogram k (k - 1) / 2 LDS increments per
-// token-layer: measured on MI355X, 0.243 ms against 0.373 ms at E = 64, top-6 (2^21 tokens x 27
-// layers), but 0.265 ms against 0.209 ms at E = 60, top-4 (3 x 2^20 tokens x 24 layers).
+// token-layer (coact.hip).  Measured on MI355X: at E = 64, top-6 (2^21 tokens x 27 layers) 0.18 ms
+// against 0.37 ms for the histogram; at E = 60, top-4 the histogram is as fast.  At E = 128, top-8
+// the four-block variant of this kernel (ten products per 64 token-layers, 160 accumulator registers,
+// two waves per SIMD) took 1.60 ms against the histogram's 1.47 ms, so only E <= 64 uses it.
 bool coact_uses_mfma(int32_t n_experts, int32_t top_k) { return n_experts <= 64 && top_k >= 5; }
 
 int coact_mfma_workgroups(int64_t total) {
-  // one wave per workgroup; about 8192 token-layers each, at most 4096 waves (16 per CU)
+  // one wave per workgroup; about 8192 token-layers each, at most 4096 waves (16 per CU, all resident)
   const int64_t want = (total + 8191) / 8192;
   return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(4096, want)));
 }
@@ -186,6 +289,9 @@ int coact_mfma_workgroups(int64_t total) {
 int launch_coact_mfma_hist(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
                            int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam, int32_t W, int32_t nbins,
                            uint32_t* partial, uint32_t* d_err, hipStream_t stream) {
+  // each wave addresses its range with 24-bit products of token-layer offsets: keep it below 2^24
+  // token-layers (at most 4096 waves, so this holds for any trace below 2^36 token-layers)
+  if ((n_tokens * n_layers + W - 1) / W >= (int64_t(1) << 24)) return TACG_E_UNSUPPORTED;
   MfmaArgs a{};
   a.trace = trace;
   a.N = n_tokens;

@@ -70,6 +70,13 @@ def _rand_trace(L, N, k, E, seed, device="cuda"):
     (256, 8, 3, [30000, 17, 25000], 13),
     (128, 8, 2, [40000, 33000], 14),
     (60, 4, 2, [50000, 20000, 1], 15),
+    # on both sides of the matrix-core threshold (E <= 64, k >= 5)
+    (65, 6, 2, [3000, 1, 2500], 16),
+    (127, 9, 2, [4100, 0, 900], 17),
+    (128, 10, 1, [6000, 70], 18),
+    (100, 7, 3, [20000, 9000], 19),
+    (64, 5, 2, [3000, 3000], 20),
+    (33, 16, 1, [2000], 21),
 ])
 def test_coact_parity(E, k, L, counts, seed):
     _say(f"coact E={E} k={k} L={L} counts={counts}")
@@ -127,7 +134,8 @@ def test_coact_repeat_is_deterministic():
 
 @pytest.mark.parametrize("E,k,counts,L", [(8, 2, [2048, 2048, 2048], 2), (100, 4, [300, 0, 513, 7], 3),
                                            (256, 8, [600, 1, 900], 2), (13, 1, [700, 300], 2),
-                                           (48, 7, [900, 0, 1500, 65], 2), (90, 6, [800, 77, 1200], 2)])
+                                           (48, 7, [900, 0, 1500, 65], 2), (90, 6, [800, 77, 1200], 2),
+                                           (128, 8, [700, 0, 1900, 3], 2)])
 def test_coact_repeated_builds_exact(E, k, counts, L):
     """Many short segments flush the workgroup triangles often; every one of repeated builds into the
     same outputs must equal the oracle (a lost or late increment at a flush would show here)."""
@@ -143,7 +151,7 @@ def test_coact_repeated_builds_exact(E, k, counts, L):
     assert _err(err) == 0
 
 
-@pytest.mark.parametrize("E,k", [(16, 4), (16, 6), (200, 8)])   # histogram, matrix-core, histogram paths
+@pytest.mark.parametrize("E,k", [(16, 4), (16, 6), (200, 8), (64, 8), (32, 5)])   # histogram / matrix-core paths
 def test_coact_data_errors_flagged(E, k):
     """Repeated and out-of-range ids are flagged; the offending token-layer is skipped, as the oracle
     skips it."""
@@ -159,7 +167,7 @@ def test_coact_data_errors_flagged(E, k):
         np.testing.assert_array_equal(_u32(D), Do)
 
 
-@pytest.mark.parametrize("E,k", [(16, 4), (16, 6)])
+@pytest.mark.parametrize("E,k", [(16, 4), (16, 6), (64, 8)])
 def test_coact_empty_trace(E, k):
     tr = torch.zeros((2, 0, k), dtype=torch.int16, device="cuda")
     D, C, err = tacg.coact_build(tr, [0, 0, 0], E)
