@@ -44,16 +44,20 @@ struct EvWs {
   int32_t* rep_list;    // [L][TACG_MAX_REPLICATED]
   int32_t* n_rep;       // [L]
   uint2* rep_info;      // [L][TACG_MAX_REPLICATED][P]  (FC mask, fallback GPU)
+  // accumulators are laid out with the placement fastest, so that a workgroup's adds for its run of
+  // placements are contiguous (coalesced atomics)
   unsigned long long* acc_home;  // [P]
   unsigned long long* acc_span;  // [P]
-  unsigned long long* acc_fam;   // [P][F]
-  uint32_t* rep_load;   // [P][L][G]
+  unsigned long long* acc_fam;   // [F][P]
+  uint32_t* rep_load;   // [L][G][P2], P2 = P rounded up to even: placement pairs share a 64-bit add
   // App. C statistics (used only by tacg_eval_trace_stats)
   uint32_t* cnt_fam;                  // [F][L][E] dispatches per expert and family
-  unsigned long long* acc_span_fam;   // [P][F] sum of |cards| over the family's token-layers
-  unsigned long long* acc_cross_fam;  // [P][F] token-layers whose cards span several bands
-  unsigned long long* acc_hmass_fam;  // [P][F] replicated-slot dispatches served in the family's band
+  unsigned long long* acc_span_fam;   // [F][P] sum of |cards| over the family's token-layers
+  unsigned long long* acc_cross_fam;  // [F][P] token-layers whose cards span several bands
+  unsigned long long* acc_hmass_fam;  // [F][P] replicated-slot dispatches served in the family's band
 };
+
+__host__ __device__ inline int32_t even_up(int32_t P) { return P + (P & 1); }
 
 EvWs carve_ev(void* ws, int32_t L, int32_t E, int32_t G, int32_t P, int32_t F, size_t* used = nullptr) {
   Carver c{static_cast<char*>(ws), 0};
@@ -63,7 +67,7 @@ EvWs carve_ev(void* ws, int32_t L, int32_t E, int32_t G, int32_t P, int32_t F, s
   r.acc_home = c.take<unsigned long long>(static_cast<size_t>(P));
   r.acc_span = c.take<unsigned long long>(static_cast<size_t>(P));
   r.acc_fam = c.take<unsigned long long>(static_cast<size_t>(P) * F);
-  r.rep_load = c.take<uint32_t>(static_cast<size_t>(P) * L * G);
+  r.rep_load = c.take<uint32_t>(static_cast<size_t>(even_up(P)) * L * G);
   r.rep_of = c.take<uint8_t>(static_cast<size_t>(L) * E);
   r.rep_list = c.take<int32_t>(static_cast<size_t>(L) * TACG_MAX_REPLICATED);
   r.n_rep = c.take<int32_t>(static_cast<size_t>(L));
@@ -112,7 +116,7 @@ __global__ __launch_bounds__(256) void ev_zero(EvArgs a) {
     w.acc_span[j] = 0;
   }
   for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.F; j += stride) w.acc_fam[j] = 0;
-  for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.L * a.G; j += stride) w.rep_load[j] = 0;
+  for (int64_t j = i; j < static_cast<int64_t>(even_up(a.P)) * a.L * a.G; j += stride) w.rep_load[j] = 0;
   if (a.stats) {
     for (int64_t j = i; j < static_cast<int64_t>(a.F) * a.L * a.E; j += stride) w.cnt_fam[j] = 0;
     for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.F; j += stride) {
@@ -523,16 +527,18 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
     for (int c = 0; c < kRcntPerThread; ++c) {
       const int i = threadIdx.x + c * kMainThreads;
       if (i < G * PW / 2) {
-        const int g = (2 * i) / PW, q = 2 * i - g * PW, p = p0 + q;
-        uint32_t* dst = a.ws.rep_load + (static_cast<int64_t>(p) * L + l) * G + g;
-        if (p < a.P && rsum[2 * c]) atomicAdd(dst, rsum[2 * c]);
-        if (p + 1 < a.P && rsum[2 * c + 1]) atomicAdd(dst + static_cast<int64_t>(L) * G, rsum[2 * c + 1]);
+        const int g = (2 * i) / PW, q = 2 * i - g * PW, p = p0 + q;  // p even
+        // placements p and p + 1 are adjacent: one 64-bit add carries both counts (each below 2^32,
+        // so nothing carries from the low half); a slot past P is padding
+        const uint64_t pair = static_cast<uint64_t>(rsum[2 * c]) | (static_cast<uint64_t>(rsum[2 * c + 1]) << 32);
+        unsigned long long* dst = reinterpret_cast<unsigned long long*>(
+            a.ws.rep_load + (static_cast<int64_t>(l) * G + g) * even_up(a.P) + p);
+        if (p < a.P && pair) atomicAdd(dst, static_cast<unsigned long long>(pair));
         if constexpr (STATS) {  // replicated-slot dispatches served inside the family's own band
           if (static_cast<uint32_t>(g) - hs < hz) {
-            unsigned long long* hm = a.ws.acc_hmass_fam + static_cast<int64_t>(p) * a.F + f;
+            unsigned long long* hm = a.ws.acc_hmass_fam + static_cast<int64_t>(f) * a.P + p;
             if (p < a.P && rsum[2 * c]) atomicAdd(hm, static_cast<unsigned long long>(rsum[2 * c]));
-            if (p + 1 < a.P && rsum[2 * c + 1])
-              atomicAdd(hm + a.F, static_cast<unsigned long long>(rsum[2 * c + 1]));
+            if (p + 1 < a.P && rsum[2 * c + 1]) atomicAdd(hm + 1, static_cast<unsigned long long>(rsum[2 * c + 1]));
           }
         }
       }
@@ -570,6 +576,9 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
   uint32_t* rcnt = lds + E * PW + 2 * TACG_MAX_REPLICATED * PW;       // [G][PW / 2] two u16 counters
   uint32_t* ecnt = rcnt + G * PW / 2;                                 // [E] dispatch counts
   uint8_t* rep_of = reinterpret_cast<uint8_t*>(ecnt + E);             // [E]
+  // [kRed][PW] per-placement cost sums of the workgroup's waves, then the sum of their n_scored
+  constexpr int kRed = STATS ? 3 : 2;  // span, home (and cross)
+  uint32_t* red = reinterpret_cast<uint32_t*>(rep_of + ((E + 255) & ~255));  // rep_of padded to 256 bytes
   const uint8_t* rep_of_g = a.ws.rep_of + static_cast<int64_t>(l) * E;
 
   // one-hot primary GPU of every expert that has a single candidate in the placement; zero for the
@@ -610,6 +619,7 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
     }
   }
   for (int i = threadIdx.x; i < G * PW / 2; i += blockDim.x) rcnt[i] = 0;
+  for (int i = threadIdx.x; i < kRed * PW + 1; i += blockDim.x) red[i] = 0;
   for (int i = threadIdx.x; i < E; i += blockDim.x) {
     rep_of[i] = rep_of_g[i];
     ecnt[i] = 0;
@@ -629,22 +639,35 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
                                       hs, hz, f, err, acc_span, acc_home, acc_cross, n_scored);
   }
 
-  // ---- flush ----
+  // ---- flush: each wave adds its per-placement costs into the workgroup's LDS sums as it finishes;
+  // then one global add per placement and accumulator, contiguous in p ----
 #pragma unroll
   for (int q = 0; q < PPL; ++q) {
-    const int p = p0 + lane * PPL + q;
+    const int c = lane * PPL + q;
+    __hip_atomic_fetch_add(&red[c], acc_span[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __hip_atomic_fetch_add(&red[PW + c], acc_home[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if constexpr (STATS)
+      __hip_atomic_fetch_add(&red[2 * PW + c], acc_cross[q], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  if constexpr (STATS) {
+    if (lane == 0) __hip_atomic_fetch_add(&red[kRed * PW], n_scored, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  }
+  barrier_after_lds_atomics();
+  for (int c = threadIdx.x; c < PW; c += blockDim.x) {
+    const int p = p0 + c;
     if (p < a.P) {
-      if (acc_span[q]) atomicAdd(&a.ws.acc_span[p], static_cast<unsigned long long>(acc_span[q]));
-      if (acc_home[q]) {
-        atomicAdd(&a.ws.acc_home[p], static_cast<unsigned long long>(acc_home[q]));
-        atomicAdd(&a.ws.acc_fam[static_cast<int64_t>(p) * a.F + f], static_cast<unsigned long long>(acc_home[q]));
+      const uint32_t span = red[c], home = red[PW + c];
+      if (span) atomicAdd(&a.ws.acc_span[p], static_cast<unsigned long long>(span));
+      if (home) {
+        atomicAdd(&a.ws.acc_home[p], static_cast<unsigned long long>(home));
+        atomicAdd(&a.ws.acc_fam[static_cast<int64_t>(f) * a.P + p], static_cast<unsigned long long>(home));
       }
       if constexpr (STATS) {
-        // |cards| - 1 summed over the wave's token-layers (each has at least one card)
-        const int64_t pf = static_cast<int64_t>(p) * a.F + f;
-        const uint32_t span = acc_span[q] - n_scored;
-        if (span) atomicAdd(&a.ws.acc_span_fam[pf], static_cast<unsigned long long>(span));
-        if (acc_cross[q]) atomicAdd(&a.ws.acc_cross_fam[pf], static_cast<unsigned long long>(acc_cross[q]));
+        // |cards| - 1 summed over the workgroup's token-layers (each has at least one card)
+        const int64_t fp = static_cast<int64_t>(f) * a.P + p;
+        const uint32_t sp = span - red[kRed * PW];
+        if (sp) atomicAdd(&a.ws.acc_span_fam[fp], static_cast<unsigned long long>(sp));
+        if (red[2 * PW + c]) atomicAdd(&a.ws.acc_cross_fam[fp], static_cast<unsigned long long>(red[2 * PW + c]));
       }
     }
   }
@@ -678,7 +701,7 @@ __global__ __launch_bounds__(256) void ev_finalize(EvArgs a, uint64_t* __restric
   barrier_after_lds_atomics();
   if (threadIdx.x < G) {
     const int64_t o = (static_cast<int64_t>(p) * L + l) * G + threadIdx.x;
-    load[o] = acc[threadIdx.x] + a.ws.rep_load[o];
+    load[o] = acc[threadIdx.x] + a.ws.rep_load[(static_cast<int64_t>(l) * G + threadIdx.x) * even_up(a.P) + p];
   }
   if (l == 0) {
     if (threadIdx.x == 0) {
@@ -687,7 +710,7 @@ __global__ __launch_bounds__(256) void ev_finalize(EvArgs a, uint64_t* __restric
     }
     if (cost_home_fam)
       for (int f = threadIdx.x; f < a.F; f += blockDim.x)
-        cost_home_fam[static_cast<int64_t>(p) * a.F + f] = a.ws.acc_fam[static_cast<int64_t>(p) * a.F + f];
+        cost_home_fam[static_cast<int64_t>(p) * a.F + f] = a.ws.acc_fam[static_cast<int64_t>(f) * a.P + p];
   }
 }
 
@@ -716,18 +739,20 @@ __global__ __launch_bounds__(256) void ev_stats(EvArgs a, uint64_t* __restrict__
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
   __syncthreads();
   if (threadIdx.x == 0) {
-    const int64_t pf = static_cast<int64_t>(p) * a.F + f;
-    hmass_fam[pf] = red[0] + red[1] + red[2] + red[3] + a.ws.acc_hmass_fam[pf];
-    span_fam[pf] = a.ws.acc_span_fam[pf];
-    cross_fam[pf] = a.ws.acc_cross_fam[pf];
+    const int64_t pf = static_cast<int64_t>(p) * a.F + f, fp = static_cast<int64_t>(f) * a.P + p;
+    hmass_fam[pf] = red[0] + red[1] + red[2] + red[3] + a.ws.acc_hmass_fam[fp];
+    span_fam[pf] = a.ws.acc_span_fam[fp];
+    cross_fam[pf] = a.ws.acc_cross_fam[fp];
   }
 }
 
 template <int K, int PPL, bool STATS>
 int launch_main(const EvArgs& a, int n_pblocks, hipStream_t stream) {
   constexpr int PW = 64 * PPL;
+  constexpr int kRed = STATS ? 3 : 2;
   const size_t lds = static_cast<size_t>(a.E) * PW * 4 + static_cast<size_t>(2) * TACG_MAX_REPLICATED * PW * 4 +
-                     static_cast<size_t>(a.G) * PW * 2 + static_cast<size_t>(a.E) * 4 + align256(a.E);
+                     static_cast<size_t>(a.G) * PW * 2 + static_cast<size_t>(a.E) * 4 + align256(a.E) +
+                     static_cast<size_t>(kRed * PW + 1) * 4;
   (void)hipFuncSetAttribute(reinterpret_cast<const void*>(&ev_main<K, PPL, STATS>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
   EvArgs b = a;
