@@ -10,7 +10,8 @@ same library before timing).
 
 Prints one JSON line.  Default workload: DeepSeek-V3-like shape (E=256, top-8, 58 MoE layers,
 16 families, 2^23 tokens per trace, 1024 placements on 32 simulated GPUs, 16 generic experts with 3
-secondaries each).  --config selects another preset.
+secondaries each).  --config selects another preset; --config all prints one line per preset.
+Every line records the seeds of its workload, the SHA-256 of its traces and the host's core counts.
 """
 from __future__ import annotations
 
@@ -26,7 +27,8 @@ sys.path.insert(0, ROOT)
 METRIC = "routed token·layers/sec (coact build) + placements×tokens/sec scored; % HBM BW"
 HBM_PEAK_GBS = 8000.0                 # MI355X HBM3E, GB/s
 N_CU, CLOCK_HZ = 256, 2.4e9
-VALU_PEAK_TOPS = N_CU * 64 * CLOCK_HZ / 1e12   # int32 lane-ops per second (64 lanes / CU / clock)
+VALU_PEAK_TOPS = N_CU * 64 * CLOCK_HZ / 1e12   # T int32 lane-ops per second (64 lanes / CU / clock)
+SINGLE_THREAD_PRESETS = ("tiny", "deepseek16b")  # presets with a one-thread oracle figure
 CALIB_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 
@@ -66,7 +68,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", default="deepseek_v3")
+    ap.add_argument("--config", default="deepseek_v3", help="a preset name, or 'all' (one JSON line per preset)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-quality", action="store_true", help="skip the untimed placement-quality context")
     ap.add_argument("--no-online", action="store_true", help="skip the decayed-load scoring measurement")
@@ -131,21 +133,40 @@ def main():
                                    "(the simulated GPU count G is a parameter of the workload, not of the launch)"}))
         sys.exit(2)
 
+    import torch
+
+    from paper_2606_01007_amd import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    names = list(synth.CONFIGS) if args.config == "all" else [args.config]
+    for name in names:
+        result = run_config(name, args, all_mode=args.config == "all")
+        print(json.dumps(result), flush=True)
+        torch.cuda.empty_cache()
+
+
+def host_info() -> dict:
+    import oracle
+    oracle.build()
+    aff = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None
+    return {"nproc": os.cpu_count(), "cpus_usable": aff, "oracle_threads": oracle.num_threads()}
+
+
+def run_config(name: str, args, all_mode: bool = False) -> dict:
     import numpy as np
     import torch
 
     import paper_2606_01007_amd as tacg
     from paper_2606_01007_amd import synth
 
-    assert torch.cuda.is_available(), "bench.py needs a GPU"
-    torch.cuda.set_device(0)
     dev = "cuda"
-    cfg = synth.CONFIGS[args.config]
+    cfg = synth.CONFIGS[name]
     t0 = time.time()
-    w = synth.make_workload(args.config, device=dev, n_tokens=args.tokens or None, layers=args.layers or None)
+    w = synth.make_workload(name, device=dev, n_tokens=args.tokens or None, layers=args.layers or None)
     torch.cuda.synchronize()
     gen_s = time.time() - t0
-    log(f"generated {args.config} in {gen_s:.1f} s")
+    log(f"generated {name} in {gen_s:.1f} s")
     ps = w.placement_sets[0]
     E, k, F = cfg.E, cfg.k, cfg.F
     L = w.trace_group.shape[0]
@@ -227,10 +248,13 @@ def main():
     trace_bytes_s = Ns * L * k * 2
     c_bytes = F * L * E * E * 4 + F * L * E * 4
     coact_gbs = (trace_bytes_g + c_bytes) / t_coact / 1e9
-    # algorithmic integer work per placement-token-layer: k table lookups, k-1 ORs of one-hot GPU masks,
-    # two popcounts and the replica resolution, about 2k + 6 lane-ops
-    valu_ops = ptl * (2 * k + 6)
-    eval_tops = valu_ops / t_eval / 1e12
+    # algorithmic integer work per placement-token-layer: k-1 ORs of one-hot GPU masks, the and-not
+    # with the anchor bit and two popcounts, k + 2 lane-ops (a lower bound for any mask-based scoring
+    # on 32-bit lanes); the wider count 2k + 6 adds the k table lookups and the replica resolution,
+    # but the lookups run on the LDS, one read serving every placement of a lane, so that count can
+    # pass the VALU peak
+    eval_tops = ptl * (k + 2) / t_eval / 1e12
+    eval_tops_wide = ptl * (2 * k + 6) / t_eval / 1e12
     result = {
         "metric": METRIC,
         "value": coact_rate,
@@ -261,19 +285,23 @@ def main():
         "reweight_ms": t_rw * 1e3,
         "jain_ms": t_jain * 1e3,
         "roofline": {"kernel": "ev_main (tacg_eval_placements)", "bound": "alu",
-                     "achieved": eval_tops, "peak": VALU_PEAK_TOPS, "unit": "TFLOP/s",
+                     "achieved": eval_tops, "peak": VALU_PEAK_TOPS, "unit": "T int32 lane-ops/s",
                      "frac": eval_tops / VALU_PEAK_TOPS,
+                     "achieved_2k_plus_6": eval_tops_wide, "frac_2k_plus_6": eval_tops_wide / VALU_PEAK_TOPS,
                      "traffic": None if reduced else measured_traffic("ev_main", cfg.name),
-                     "note": "2k + 6 int32 lane-ops per placement-token-layer (k table lookups, k-1 ORs "
-                             "of one-hot GPU masks, two popcounts, replica resolution); the stricter "
-                             "k + 2 count (ORs, and-not, popcounts only) gives frac x (k+2)/(2k+6); "
-                             "peak = 256 CUs x 64 lanes x 2.4 GHz"},
-        "roofline_coact": {"kernel": "coact_hist + coact_reduce (tacg_coact_build)", "bound": "hbm",
+                     "note": "achieved/frac: k + 2 int32 lane-ops per placement-token-layer (k-1 ORs of "
+                             "one-hot GPU masks, the and-not with the anchor bit, two popcounts); "
+                             "*_2k_plus_6: also the k table lookups and the replica resolution, which "
+                             "run partly on the LDS (one read serves all placements of a lane), so it "
+                             "can exceed 1; peak = 256 CUs x 64 lanes x 2.4 GHz"},
+        "roofline_coact": {"kernel": ("coact_mfma" if E <= 64 and k >= 5 else "coact_hist")
+                                     + " + coact_reduce (tacg_coact_build)", "bound": "hbm",
                            "achieved": coact_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": coact_gbs / HBM_PEAK_GBS,
                            "traffic": None if reduced else measured_traffic("coact_build", cfg.name),
                            "note": "algorithmic bytes: the int16 trace once + dense C and D written"},
         "gen_s": gen_s,
+        "seeds": synth.workload_seeds(cfg),
     }
 
     log(f"timed {args.steps} steps: {wall / args.steps * 1e3:.1f} ms/step")
@@ -282,9 +310,26 @@ def main():
         result["placement_quality"] = placement_quality(w, ps, cfg, D, C, err)
     if not args.no_online:
         result["online_scoring"] = online_scoring(w, ps, cfg, prim, sec, err, args.online_tokens)
+    del D, C, ws_c, ws_r, ws_e, out
+    torch.cuda.empty_cache()
+    # host copies of the traces: their SHA-256 and the oracle's input
+    t0 = time.time()
+    tg = w.trace_group.cpu().numpy()
+    ts = tg if w.trace_serve is w.trace_group else w.trace_serve.cpu().numpy()
+    result["trace_sha256"] = {"grouping": synth.trace_digest(tg),
+                              "serving": synth.trace_digest(ts) if ts is not tg else "same as grouping"}
+    result["host"] = host_info()
+    log(f"trace digests in {time.time() - t0:.1f} s")
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, ps, cfg, args.cpu_layers)
-    print(json.dumps(result), flush=True)
+        result["cpu_baseline"] = cpu_baseline(w, tg, ts, ps, cfg, args.cpu_layers)
+        st = {}
+        for sname in SINGLE_THREAD_PRESETS:
+            if all_mode and sname != name:
+                continue  # with --config all each of these presets reports its own
+            st[sname] = single_thread_oracle(sname, w if sname == name else None)
+        if st:
+            result["cpu_baseline"]["single_thread"] = st
+    return result
 
 
 def aux_timings(D, C, prim, cfg, G, reps=5):
@@ -400,31 +445,29 @@ def placement_quality(w, ps, cfg, D, C, err):
             "host_s": time.time() - t0}
 
 
-def cpu_baseline(w, ps, cfg, cpu_layers):
+def cpu_baseline(w, tg, ts, ps, cfg, cpu_layers):
     """The oracle as it stands, on this host's cores: the whole co-activation build of the grouping
     trace, and the first three placements scored over the serving trace (scaled to placements x
-    tokens / s); about 15 s of CPU work at the full DeepSeek-V3-like workload."""
+    tokens / s); about 15 s of CPU work at the full DeepSeek-V3-like workload.  tg, ts: host copies
+    of the two traces."""
     import numpy as np
     import oracle
 
     oracle.build()
     log("cpu baseline: oracle co-activation build")
-    tg = w.trace_group.cpu().numpy()
     t0 = time.perf_counter()
     _, _, e1 = oracle.coact(tg, w.fam_off_group, cfg.E)
     t_coact = time.perf_counter() - t0
-    del tg
-    ts = w.trace_serve.cpu().numpy()
     Ls = ts.shape[0] if cpu_layers <= 0 else min(cpu_layers, ts.shape[0])
     ts = np.ascontiguousarray(ts[:Ls])
     G = ps["n_gpus"]
-    sec = ps["secondary"][:, :Ls] if ps["secondary"] is not None else None
-    prim = ps["primary"][:, :Ls]
+    n_p = min(3, ps["primary"].shape[0])
+    sec = ps["secondary"][:n_p, :Ls] if ps["secondary"] is not None else None
+    prim = ps["primary"][:n_p, :Ls]
     ref = None
     if sec is not None:
         Ds, _, _ = oracle.coact(ts, w.fam_off_serve, cfg.E)
         ref = oracle.placement_load(Ds, prim, G)
-    n_p = min(3, prim.shape[0])
     log(f"cpu baseline: oracle scoring of {n_p} placements")
     t0 = time.perf_counter()
     r = oracle.score(ts, w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], G, prim, sec, ref, (3, 20),
@@ -440,6 +483,50 @@ def cpu_baseline(w, ps, cfg, cpu_layers):
             "scoring_value": n_p * Ns * Ls / w.trace_serve.shape[0] / t_score if Ls else None,
             "scoring_unit": "placements×tokens/s (over all layers, scaled from the sample)",
             "err": int(e1) | int(r["err"])}
+
+
+def single_thread_oracle(name: str, w=None, device: str = "cuda") -> dict:
+    """The oracle on one thread, on a preset's full grouping trace (co-activation build) and one
+    placement scored over its serving trace: the per-core figure beside the all-cores baseline."""
+    import numpy as np
+    import oracle
+
+    from paper_2606_01007_amd import synth
+
+    cfg = synth.CONFIGS[name]
+    if w is None:
+        w = synth.make_workload(name, device=device)
+    tg = w.trace_group.cpu().numpy()
+    ts = w.trace_serve.cpu().numpy()
+    ps = w.placement_sets[0]
+    G = ps["n_gpus"]
+    prim = ps["primary"][:1]
+    sec = ps["secondary"][:1] if ps["secondary"] is not None else None
+    oracle.build()
+    threads = oracle.num_threads()
+    oracle.set_num_threads(1)
+    try:
+        log(f"cpu baseline: one-thread oracle on {name}")
+        t0 = time.perf_counter()
+        _, _, e1 = oracle.coact(tg, w.fam_off_group, cfg.E)
+        t_coact = time.perf_counter() - t0
+        ref = None
+        if sec is not None:
+            Ds, _, _ = oracle.coact(ts, w.fam_off_serve, cfg.E)
+            ref = oracle.placement_load(Ds, prim, G)
+        t0 = time.perf_counter()
+        r = oracle.score(ts, w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], G, prim, sec, ref,
+                         (3, 20))
+        t_score = time.perf_counter() - t0
+    finally:
+        oracle.set_num_threads(threads)
+    L, Ng, Ns = tg.shape[0], tg.shape[1], ts.shape[1]
+    return {"cores": 1, "coact_value": Ng * L / t_coact, "coact_unit": "routed token·layers/s",
+            "scoring_value": Ns / t_score, "scoring_unit": "placements×tokens/s",
+            "sample": f"co-activation build of the whole grouping trace ({Ng} tokens x {L} layers, "
+                      f"{t_coact:.2f} s); placement 0 scored over the serving trace ({Ns} tokens x {L} layers, "
+                      f"{t_score:.2f} s)",
+            "trace_sha256": synth.trace_digest(tg), "err": int(e1) | int(r["err"])}
 
 
 if __name__ == "__main__":

@@ -62,12 +62,22 @@ def build(force: bool = False) -> str:
     return _LIB
 
 
+def build_sanitized(path: str) -> str:
+    """Compile tacg_oracle.c with AddressSanitizer and UndefinedBehaviorSanitizer into `path` (for the
+    CPU sanitizer tests: load it with TACG_ORACLE_LIBRARY=path and gcc's libasan preloaded)."""
+    subprocess.run(["gcc", "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                    "-fno-sanitize-recover=undefined", "-fopenmp", "-fPIC", "-shared", "-Wall", "-ffp-contract=off",
+                    "-o", path, _SRC, "-lm"], check=True)
+    return path
+
+
 def _load():
     global _lib
     with _lock:
         if _lib is None:
-            build()
-            lib = ctypes.CDLL(_LIB)
+            # TACG_ORACLE_LIBRARY names another build of tacg_oracle.c (a sanitized one, for instance)
+            path = os.environ.get("TACG_ORACLE_LIBRARY") or build()
+            lib = ctypes.CDLL(path)
             P = ctypes.c_void_p
             i32, i64 = ctypes.c_int32, ctypes.c_int64
             lib.oracle_coact_segment.argtypes = [P, i64, i32, i32, i32, i64, i64, P, P]
@@ -81,6 +91,8 @@ def _load():
                                                 P, P, i32, ctypes.c_double, i32, i32, P, P, P, P, P, P]
             lib.oracle_score_online.restype = ctypes.c_int
             lib.oracle_num_threads.restype = ctypes.c_int
+            lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+            lib.oracle_set_num_threads.restype = None
             _lib = lib
     return _lib
 
@@ -98,6 +110,11 @@ def _np(x, dtype):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops from now on (timing only; results do not depend on it)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 # ------------------------------------------------------------------------------------------------

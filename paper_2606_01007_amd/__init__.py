@@ -26,7 +26,8 @@ import numpy as np
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libtacg.so")
+# TACG_LIBRARY names another build of the library to load (a host-sanitized build, for instance)
+LIB_PATH = os.environ.get("TACG_LIBRARY") or os.path.join(_PKG, "libtacg.so")
 
 OK, E_INVAL, E_UNSUPPORTED, E_DEVICE, E_SCRATCH = 0, -1, -2, -3, -4
 NOALLOC_SCRATCH_BYTES = 32 << 20

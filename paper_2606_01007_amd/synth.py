@@ -336,12 +336,25 @@ def make_workload(name: str, device="cpu", n_tokens: Optional[int] = None, n_pla
     return Workload(cfg, tr_g, off_g, tr_s, off_s, pl, sets)
 
 
-def trace_digest(trace: torch.Tensor) -> str:
-    """SHA-256 of the trace bytes (recorded with results)."""
+def trace_digest(trace) -> str:
+    """SHA-256 of the trace bytes (recorded with results); a torch tensor or a host numpy array."""
     h = hashlib.sha256()
-    t = trace.detach().to("cpu").contiguous().view(torch.uint8).numpy()
+    if isinstance(trace, torch.Tensor):
+        t = trace.detach().to("cpu").contiguous().view(torch.uint8).numpy()
+    else:
+        t = np.ascontiguousarray(trace).view(np.uint8)
     step = 1 << 28
     flat = t.reshape(-1)
     for i in range(0, flat.size, step):
         h.update(flat[i:i + step].tobytes())
     return h.hexdigest()
+
+
+def workload_seeds(cfg: TraceConfig, placement_seed_offset: int = 0) -> dict:
+    """The seeds make_workload draws a preset from (recorded with results)."""
+    out = {"logits_and_grouping_trace": cfg.seed,
+           "serving_trace": cfg.seed_serve if cfg.serve_mix != "same" else cfg.seed}
+    for i, _ in enumerate(cfg.placements):
+        out[f"placements_{i}"] = cfg.seed + 1000 * (i + 1) + placement_seed_offset
+        out[f"secondaries_{i}"] = cfg.seed + 2000 * (i + 1) + placement_seed_offset
+    return out

@@ -65,3 +65,34 @@ def test_traffic_needs_the_calibration_copy(tmp_path, monkeypatch):
     _counters(write, "WRITE_SIZE", [("__amd_rocclr_copyBuffer", 1048576.0)])
     with pytest.raises(SystemExit):
         bench.write_traffic(str(fetch), str(write), "deepseek_v3")
+
+
+def test_single_thread_oracle_record():
+    """The one-thread oracle figure of a preset: whole grouping trace and one placement, on one
+    thread, with the trace's digest; the oracle's thread count is restored afterwards."""
+    import oracle
+    from paper_2606_01007_amd import synth
+
+    oracle.build()
+    before = oracle.num_threads()
+    rec = bench.single_thread_oracle("tiny", device="cpu")
+    assert oracle.num_threads() == before
+    assert rec["cores"] == 1 and rec["err"] == 0
+    assert rec["coact_value"] > 0 and rec["scoring_value"] > 0
+    w = synth.make_workload("tiny")
+    assert rec["trace_sha256"] == synth.trace_digest(w.trace_group)
+    assert "6144 tokens x 2 layers" in rec["sample"]
+
+
+def test_workload_seeds_are_the_generators_seeds():
+    from paper_2606_01007_amd import synth
+
+    s = synth.workload_seeds(synth.CONFIGS["qwen15"])
+    assert s == {"logits_and_grouping_trace": 103, "serving_trace": 103, "placements_0": 1103,
+                 "secondaries_0": 2103, "placements_1": 2103, "secondaries_1": 4103}
+    s = synth.workload_seeds(synth.CONFIGS["deepseek_v3"])
+    assert s["serving_trace"] == 205 and s["placements_0"] == 1105
+    # the recorded seeds regenerate the recorded placements
+    w = synth.make_workload("tiny")
+    p = synth.random_placements(16, 2, 8, 4, 2, synth.workload_seeds(synth.CONFIGS["tiny"])["placements_0"])
+    assert (p == w.placement_sets[0]["primary"]).all()
