@@ -17,7 +17,7 @@
 //     workspace (slot indices are unique because both w and s grow along x), then zeroes it.
 //   * A second kernel, one workgroup per segment, sums the partial slots of the workgroups that
 //     touched the segment and writes the dense symmetric C (diagonal = D) and D.
-//   * At E <= 64 and k >= 5 the partial slots come from 4-bit matrix products instead
+//   * At E <= 64 and k >= 4 the partial slots come from 4-bit matrix products instead
 //     (coact_mfma.hip), with the same split of x, the same slots and the same reduction.
 #include "tacg_internal.h"
 

@@ -11,14 +11,22 @@
 // the reduction are shared).  The ids of the next four batches are in flight while one is counted.
 // Per batch of 64 token-layers (one per lane):
 //   * each lane forms its token's one-hot row in registers: a 64-bit mask of its ids (which also
-//     validates them: a repeated id leaves fewer than k bits), spread to one e2m1 nibble per expert
-//     (0x1 = 0.5, so a product is 0.25 and every float32 partial sum is exact);
+//     validates them: a repeated id leaves fewer than k bits, an id of E or more sets a bit outside
+//     the lane's valid set or a bit above bit 5 of its raw word), turned into one e2m1 nibble per
+//     expert (0x1 = 0.5, so a product is 0.25 and every float32 partial sum is exact).  The nibbles
+//     come from byte permutes used as a four-entry table: selector byte j = two mask bits, output
+//     byte j = those two bits as two nibbles, so a row of 32 experts costs four permutes, four ANDs
+//     and three shifts.  For that, row position n holds the mask bit relabel(n), where relabel
+//     swaps bit fields 4:3 and 2:1 of the 6-bit index (an involution that keeps bit 5, so both
+//     32-expert blocks keep their experts); the Gram matrix is thus counted over relabelled experts
+//     and mapped back when the triangle is written;
 //   * the lane stores the row (16 NB bytes, token-major) into a wave-private LDS tile with 16-byte
 //     writes.  The 8-byte chunks of a row (16 experts each) sit at positions permuted by the row
 //     number (chunk c of row j at c ^ s(j)), which makes the reads below bank-conflict-free, and
 //     the lanes whose rows share banks write their 16-byte parts in different orders (part q ^ g(j)
 //     in store q), which makes the stores conflict-free; both permutations are XOR constants per
-//     lane, applied to the ids before the mask is formed, so they cost nothing per token;
+//     lane (relabelled like the ids), applied to the ids before the mask is formed, so they cost
+//     nothing per token;
 //   * ds_read_b64_tr_b4 reads 16 rows x 16 nibbles per group of 16 lanes and hands lane i the
 //     nibbles of column i: two such reads give lane l the 32 nibbles of expert 32 b + l % 32 over
 //     tokens 32 (l / 32) .. + 31 of the batch.  That fragment is both the A operand (row of R^T) and
@@ -58,14 +66,22 @@ __device__ __forceinline__ uint32_t tri_bin(uint32_t m, uint32_t n, uint32_t E) 
 }
 
 // Write the strict upper triangle of one 32 x 32 accumulator block (bi, bj).  Accumulator register r
-// of lane l holds row 8 (r / 4) + 4 (l / 32) + r % 4 and column l % 32 of the block, as 0.25 x count.
+// of lane l holds row 8 (r / 4) + 4 (l / 32) + r % 4 and column l % 32 of the block, as 0.25 x count;
+// row and column positions are relabelled experts.
+// Expert index <-> row position (see the file comment): swap bits 4:3 with bits 2:1.
+__device__ __forceinline__ uint32_t relabel(uint32_t x) {
+  return (x & 0x21u) | ((x & 0x18u) >> 2) | ((x & 0x06u) << 2);
+}
+
 __device__ __forceinline__ void store_block(const v16f& acc, int bi, int bj, int lane, uint32_t E,
                                             uint32_t* __restrict__ dst) {
   const uint32_t n = 32u * bj + (lane & 31);
+  const uint32_t en = relabel(n);
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const uint32_t m = 32u * bi + 8u * (r >> 2) + 4u * (lane >> 5) + (r & 3);
-    if (m < n && n < E) dst[tri_bin(m, n, E)] = static_cast<uint32_t>(acc[r] * 4.0f);
+    const uint32_t em = relabel(m);
+    if (m < n && em < E && en < E) dst[tri_bin(min(em, en), max(em, en), E)] = static_cast<uint32_t>(acc[r] * 4.0f);
   }
 }
 
@@ -83,18 +99,22 @@ struct Raw {
       for (int q = 0; q < kWords; ++q) w[q] = static_cast<uint16_t>(__builtin_nontemporal_load(p + q));
     }
   }
+  __device__ __forceinline__ uint32_t any_id_bits() const {  // OR of the raw words
+    uint32_t o = 0;
+#pragma unroll
+    for (int q = 0; q < kWords; ++q) o |= w[q];
+    return o;
+  }
   __device__ __forceinline__ uint32_t id(int s) const {  // negative ids become >= 32768 >= E
     if constexpr (K % 2 == 0) return (s & 1) ? (w[s >> 1] >> 16) : (w[s >> 1] & 0xffffu);
     else return w[s];
   }
 };
 
-// Eight one-hot bits -> eight nibbles of value 1 (bit n to bit 4 n).
-__device__ __forceinline__ uint32_t spread_nibbles(uint32_t x) {
-  x = (x | (x << 12)) & 0x000F000Fu;
-  x = (x | (x << 6)) & 0x03030303u;
-  x = (x | (x << 3)) & 0x11111111u;
-  return x;
+// Byte permute as a table lookup: selector byte j in 0..3 picks byte j of {0x00, 0x01, 0x10, 0x11},
+// so two mask bits (bits 0 and 1 of selector byte j) become two nibbles of value 1 in output byte j.
+__device__ __forceinline__ uint32_t nibble_pairs(uint32_t sel, uint32_t keep) {
+  return __builtin_amdgcn_perm(0u, 0x11100100u, sel & keep);
 }
 
 constexpr int kDepth = 4;  // batches of ids in flight per lane (even: steps alternate the two tiles)
@@ -142,7 +162,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
   // t ^ 2 g(j), i.e. logical chunk t ^ 2 g(j) ^ s(j): the ids are XOR-ed with that constant
   const uint32_t sw_row = (static_cast<uint32_t>(lane) >> kSwShift) & (kChunks - 1);
   const uint32_t part_row = (static_cast<uint32_t>(lane) >> kPartShift) & (NB - 1);
-  const uint32_t id_xor = (sw_row ^ (part_row << 1)) << 4;
+  const uint32_t id_xor = relabel((sw_row ^ (part_row << 1)) << 4);
+  // mask bits b whose expert b ^ id_xor is >= E (E <= 64; id_xor has bits 2 and 5 only)
+  uint64_t nv = E >= 64u ? 0ull : (~0ull << E);
+  if (id_xor & 4u) nv = ((nv & 0x0f0f0f0f0f0f0f0full) << 4) | ((nv >> 4) & 0x0f0f0f0f0f0f0f0full);
+  if (id_xor & 32u) nv = (nv << 32) | (nv >> 32);
+  const uint32_t nv_lo = static_cast<uint32_t>(nv), nv_hi = static_cast<uint32_t>(nv >> 32);
   const uint32_t row_off = static_cast<uint32_t>(lane) * kRowBytes;
   // transposed reads: lane l = 16 g + i reads, for block b and half r, the chunk of experts
   // 32 b + 16 (g & 1) .. + 15 of row j = 32 (g >> 1) + 16 r + i
@@ -194,36 +219,33 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     for (uint32_t rb = 0; rb < n; rb += 64 * kDepth) {
 #pragma unroll
       for (int d = 0; d < kDepth; ++d) {
-        const uint32_t r = rb + 64u * d + lane;
-        // one-hot mask of the ids in register order (the 64-bit shift uses the low six bits of its
-        // amount); validity: every id below E, k distinct ids
+        const uint32_t base = rb + 64u * d;  // batch-uniform
+        // one-hot mask of the ids (the 64-bit shift uses the low six bits of its amount)
         uint64_t m = 0;
-        uint32_t idmax = 0;
 #pragma unroll
-        for (int s = 0; s < K; ++s) {
-          const uint32_t id = ring[d].id(s);
-          idmax = max(idmax, id);
-          m |= 1ull << (id ^ id_xor);
-        }
-        const bool in_seg = r < n;
-        const bool range_bad = idmax >= E;
-        const bool dup = __builtin_popcountll(m) != K;
+        for (int s = 0; s < K; ++s) m |= 1ull << (ring[d].id(s) ^ id_xor);
+        const uint32_t m_lo = static_cast<uint32_t>(m), m_hi = static_cast<uint32_t>(m >> 32);
+        const bool in_seg = lane < static_cast<int>(n - base);
+        const bool range_bad = ((ring[d].any_id_bits() & 0xffc0ffc0u) | (m_lo & nv_lo) | (m_hi & nv_hi)) != 0u;
+        const bool dup = __popc(m_lo) + __popc(m_hi) != K;
         err |= (in_seg && range_bad) ? TACG_ERR_ID_RANGE : 0u;
         err |= (in_seg && !range_bad && dup) ? TACG_ERR_ID_DUP : 0u;
-        if (!in_seg || range_bad || dup) m = 0;  // an invalid token-layer is flagged and not counted
-        ring[d].fetch(segp + __umul24(min(r + 64u * kDepth, nlast), static_cast<uint32_t>(K)));
-        const bool active = rb + 64u * d < n;  // batch-uniform
+        // an invalid token-layer is flagged and not counted
+        const uint32_t keep = (!in_seg || range_bad || dup) ? 0u : 0x03030303u;
+        ring[d].fetch(reinterpret_cast<const int16_t*>(reinterpret_cast<const char*>(segp) +
+                      __umul24(min(lane + (base + 64u * kDepth), nlast), static_cast<uint32_t>(2 * K))));
+        const bool active = base < n;  // batch-uniform
         const uint32_t kBuf = (d & 1) * kTileBytes;
         if (active) {
           uint8_t* rowp = tile + kBuf + row_off;
 #pragma unroll
           for (int q = 0; q < NB; ++q) {  // register part q (32 experts) to the row's part q ^ g(j)
-            const uint32_t src = static_cast<uint32_t>(m >> (32 * q));
+            const uint32_t src = q == 0 ? m_lo : m_hi;
             u32x4 v;
-            v.x = spread_nibbles(src & 0xffu);
-            v.y = spread_nibbles((src >> 8) & 0xffu);
-            v.z = spread_nibbles((src >> 16) & 0xffu);
-            v.w = spread_nibbles(src >> 24);
+            v.x = nibble_pairs(src, keep);
+            v.y = nibble_pairs(src >> 2, keep);
+            v.z = nibble_pairs(src >> 4, keep);
+            v.w = nibble_pairs(src >> 6, keep);
             *reinterpret_cast<u32x4*>(rowp + 16 * (q ^ part_row)) = v;
           }
         }
@@ -252,12 +274,15 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
     // hoisting all 48 of them out of the segment loop into registers
     uint32_t Es = E;
     __asm__ __volatile__("" : "+s"(Es));
+    // likewise an opaque copy of the lane for the relabelled bin indices
+    int ln = lane;
+    __asm__ __volatile__("" : "+v"(ln));
     {
       int b = 0;
 #pragma unroll
       for (int bi = 0; bi < NB; ++bi) {
 #pragma unroll
-        for (int bj = bi; bj < NB; ++bj) store_block(acc[b++], bi, bj, lane, Es, dst);
+        for (int bj = bi; bj < NB; ++bj) store_block(acc[b++], bi, bj, ln, Es, dst);
       }
     }
     pos = stop;
@@ -274,11 +299,12 @@ void launch_k(const MfmaArgs& a, hipStream_t stream) {
 }  // namespace
 
 // The matrix path costs about the same at any k, the histogram k (k - 1) / 2 LDS increments per
-// token-layer (coact.hip).  Measured on MI355X: at E = 64, top-6 (2^21 tokens x 27 layers) 0.18 ms
-// against 0.37 ms for the histogram; at E = 60, top-4 the histogram is as fast.  At E = 128, top-8
-// the four-block variant of this kernel (ten products per 64 token-layers, 160 accumulator registers,
-// two waves per SIMD) took 1.60 ms against the histogram's 1.47 ms, so only E <= 64 uses it.
-bool coact_uses_mfma(int32_t n_experts, int32_t top_k) { return n_experts <= 64 && top_k >= 5; }
+// token-layer (coact.hip).  Measured on MI355X (kernel averages): at E = 64, top-6 (2^21 tokens x 27
+// layers) 143 us against 0.37 ms for the histogram; at E = 60, top-4 (2^22 tokens x 24 layers) 164 us
+// against 184 us.  At E = 128, top-8 the four-block variant of this kernel (ten products per 64
+// token-layers, 160 accumulator registers, two waves per SIMD) took 1.60 ms against the histogram's
+// 1.47 ms, so only E <= 64 uses it.
+bool coact_uses_mfma(int32_t n_experts, int32_t top_k) { return n_experts <= 64 && top_k >= 4; }
 
 int coact_mfma_workgroups(int64_t total) {
   // one wave per workgroup; about 8192 token-layers each, at most 4096 waves (16 per CU, all resident)

@@ -70,13 +70,17 @@ def _rand_trace(L, N, k, E, seed, device="cuda"):
     (256, 8, 3, [30000, 17, 25000], 13),
     (128, 8, 2, [40000, 33000], 14),
     (60, 4, 2, [50000, 20000, 1], 15),
-    # on both sides of the matrix-core threshold (E <= 64, k >= 5)
+    # on both sides of the matrix-core threshold (E <= 64, k >= 4)
     (65, 6, 2, [3000, 1, 2500], 16),
     (127, 9, 2, [4100, 0, 900], 17),
     (128, 10, 1, [6000, 70], 18),
     (100, 7, 3, [20000, 9000], 19),
     (64, 5, 2, [3000, 3000], 20),
     (33, 16, 1, [2000], 21),
+    (64, 3, 2, [4000, 900], 22),
+    (64, 4, 2, [4000, 900, 3], 23),
+    (32, 4, 3, [2500, 0, 1200], 24),
+    (20, 4, 2, [3100, 77], 25),
 ])
 def test_coact_parity(E, k, L, counts, seed):
     _say(f"coact E={E} k={k} L={L} counts={counts}")
