@@ -295,7 +295,7 @@ def run_config(name: str, args, all_mode: bool = False) -> dict:
                              "at four placements per lane (E <= 64) frac can exceed 1; *_k_plus_2: only "
                              "the ORs, the and-not with the anchor bit and the two popcounts, a lower "
                              "bound for any mask-based scoring; peak = 256 CUs x 64 lanes x 2.4 GHz"},
-        "roofline_coact": {"kernel": ("coact_mfma" if E <= 64 and k >= 4 else "coact_hist")
+        "roofline_coact": {"kernel": ("coact_mfma" if tacg.coact_uses_matrix_cores(E, k) else "coact_hist")
                                      + " + coact_reduce (tacg_coact_build)", "bound": "hbm",
                            "achieved": coact_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": coact_gbs / HBM_PEAK_GBS,

@@ -82,6 +82,14 @@ size_t tacg_coact_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t to
                                   int32_t n_fam);
 
 /*
+ * Which kernel tacg_coact_build runs for n_experts experts and top_k ids per token-layer: 1 when the
+ * partial counts come from 4-bit one-hot matrix products on the matrix cores (E <= 64 with k >= 4,
+ * E <= 128 with 8 <= k <= 12), 0 for the LDS pair histogram; the counts are identical either way.
+ * A host-only query (no device work); 0 for sizes tacg_coact_build rejects.
+ */
+int tacg_coact_uses_matrix_cores(int32_t n_experts, int32_t top_k);
+
+/*
  * Family preferences and the task-modulated co-activation graph (Sec. 3.3, eqs.
  * usage-coact-advantage, coact-advantage, zscore, soft-score, family-pref, same-family-kernel and
  * task-modulated-graph).  From the counts of tacg_coact_build, per layer l:

@@ -58,6 +58,8 @@ def lib():
             L.tacg_coact_build.argtypes = [P, i64, i32, i32, i32, P, i32, P, P, u32, P, P, sz, P]
             L.tacg_coact_workspace_bytes.argtypes = [i64, i32, i32, i32, i32]
             L.tacg_coact_workspace_bytes.restype = sz
+            L.tacg_coact_uses_matrix_cores.argtypes = [i32, i32]
+            L.tacg_coact_uses_matrix_cores.restype = ctypes.c_int
             L.tacg_reweight.argtypes = [P, P, i32, i32, i32, i32, f64, f64, f64, P, P, P, P, sz, P]
             L.tacg_reweight_workspace_bytes.argtypes = [i32, i32, i32]
             L.tacg_reweight_workspace_bytes.restype = sz
@@ -165,6 +167,11 @@ def _err_tensor(device) -> torch.Tensor:
 
 
 # ------------------------------------------------------------------------------------------------
+def coact_uses_matrix_cores(n_experts: int, top_k: int) -> bool:
+    """Whether tacg_coact_build counts this shape on the matrix cores (else the LDS pair histogram)."""
+    return bool(lib().tacg_coact_uses_matrix_cores(int(n_experts), int(top_k)))
+
+
 def coact_build(trace: torch.Tensor, fam_off, n_experts: int, D: Optional[torch.Tensor] = None,
                 C: Optional[torch.Tensor] = None, accumulate: bool = False, ws: Optional[torch.Tensor] = None,
                 err: Optional[torch.Tensor] = None, stream=None):

@@ -39,6 +39,12 @@ size_t tacg_coact_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t to
   return tacg::align256(slots * tacg::coact_bins(n_experts, top_k) * sizeof(uint32_t));
 }
 
+int tacg_coact_uses_matrix_cores(int32_t n_experts, int32_t top_k) {
+  if (n_experts < 1 || n_experts > TACG_MAX_EXPERTS || top_k < 1 || top_k > TACG_MAX_TOPK) return 0;
+  if (top_k > n_experts) return 0;
+  return tacg::coact_uses_mfma(n_experts, top_k) ? 1 : 0;
+}
+
 int tacg_coact_build(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k, int32_t n_experts,
                      const int64_t* fam_off_host, int32_t n_fam, uint32_t* D, uint32_t* C, uint32_t flags,
                      uint32_t* d_err, void* workspace, size_t workspace_bytes, void* hip_stream) {

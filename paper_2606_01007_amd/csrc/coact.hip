@@ -17,8 +17,9 @@
 //     workspace (slot indices are unique because both w and s grow along x), then zeroes it.
 //   * A second kernel, one workgroup per segment, sums the partial slots of the workgroups that
 //     touched the segment and writes the dense symmetric C (diagonal = D) and D.
-//   * At E <= 64 and k >= 4 the partial slots come from 4-bit matrix products instead
-//     (coact_mfma.hip), with the same split of x, the same slots and the same reduction.
+//   * At E <= 64 with k >= 4, and at E <= 128 with 8 <= k <= 12, the partial slots come from 4-bit
+//     matrix products instead (coact_mfma.hip), with the same split of x, the same slots and the
+//     same reduction.
 #include "tacg_internal.h"
 
 namespace tacg {
@@ -121,6 +122,16 @@ struct RawIds {
   }
 };
 
+constexpr uint64_t kOddLanes = 0xaaaaaaaaaaaaaaaaull;  // lanes with bit 0 set
+constexpr uint64_t kLaneBit1 = 0xccccccccccccccccull;  // lanes with bit 1 set
+
+// Per-lane choice from a wave-uniform lane mask: b in the lanes whose mask bit is set, else a.
+__device__ __forceinline__ uint32_t lane_select(uint32_t a, uint32_t b, uint64_t lanes) {
+  uint32_t r;
+  asm("v_cndmask_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "s"(lanes));
+  return r;
+}
+
 // Count one token-layer into the workgroup's triangle (see the file comment).
 template <int K>
 __device__ __forceinline__ void count_token(const RawIds<K>& raw, bool valid, uint32_t* hist, uint32_t E,
@@ -168,16 +179,33 @@ __device__ __forceinline__ void count_token(const RawIds<K>& raw, bool valid, ui
 #pragma unroll
           for (int j = i + 1; j < K; ++j) off[n++] = rb[i] + 4u * v[j];
         }
-        const bool rev = (threadIdx.x & 1u) != 0u;
-        const bool rot = (threadIdx.x & 2u) != 0u;
+        if constexpr (K == 8) {
+          const bool rev = (threadIdx.x & 1u) != 0u;
+          const bool rot = (threadIdx.x & 2u) != 0u;
 #pragma unroll
-        for (int q = 0; q < NP; ++q) {
-          const int q2 = (q + NP / 2) % NP;
-          const uint32_t x = rev ? off[NP - 1 - q] : off[q];
-          const uint32_t y = rev ? off[NP - 1 - q2] : off[q2];
-          uint32_t* cell = reinterpret_cast<uint32_t*>(__builtin_assume_aligned(
-              reinterpret_cast<char*>(hist) + (rot ? y : x), 4));
-          __hip_atomic_fetch_add(cell, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          for (int q = 0; q < NP; ++q) {
+            const int q2 = (q + NP / 2) % NP;
+            const uint32_t x = rev ? off[NP - 1 - q] : off[q];
+            const uint32_t y = rev ? off[NP - 1 - q2] : off[q2];
+            uint32_t* cell = reinterpret_cast<uint32_t*>(__builtin_assume_aligned(
+                reinterpret_cast<char*>(hist) + (rot ? y : x), 4));
+            __hip_atomic_fetch_add(cell, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          }
+        } else {
+          // At top-6 and top-7 the plain selects above were turned into selects of array indices
+          // and then into chains of selects (about 220 and 430 VALU instructions per token-layer
+          // instead of about 36 and 48; 2.5x and 3.5x slower at E = 256).  Here the selects take
+          // their lane masks from constant SGPR pairs, two per pair.  At top-8 the compiler keeps
+          // two selects per pair by itself, and its schedule measured 0.7 % faster.
+          uint32_t x[NP];
+#pragma unroll
+          for (int q = 0; q < NP; ++q) x[q] = lane_select(off[q], off[NP - 1 - q], kOddLanes);
+#pragma unroll
+          for (int q = 0; q < NP; ++q) {
+            uint32_t* cell = reinterpret_cast<uint32_t*>(__builtin_assume_aligned(
+                reinterpret_cast<char*>(hist) + lane_select(x[q], x[(q + NP / 2) % NP], kLaneBit1), 4));
+            __hip_atomic_fetch_add(cell, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+          }
         }
       } else {
 #pragma unroll
@@ -382,7 +410,7 @@ size_t coact_bins(int32_t n_experts, int32_t top_k) {
 }
 
 int coact_num_workgroups(int64_t total, int32_t n_experts, int32_t top_k) {
-  if (coact_uses_mfma(n_experts, top_k)) return coact_mfma_workgroups(total);
+  if (coact_uses_mfma(n_experts, top_k)) return coact_mfma_workgroups(total, n_experts);
   // E > 128: the triangle needs more than half of the 160 KB LDS, so one 1024-thread workgroup per
   // CU; otherwise four 512-thread workgroups per CU (the same 32 waves, with four private triangles)
   const int64_t cap = (n_experts > kCoactSmallE) ? 256 : 1024;

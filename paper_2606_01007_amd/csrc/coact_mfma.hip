@@ -2,9 +2,10 @@
 //
 // For the tokens of one (family, layer) segment, C = R^T R where R[t][e] = 1 when token t selected
 // expert e (Sec. 3.3: C counts the tokens that chose both experts).  With E <= 32 NB the Gram matrix
-// has NB x NB blocks of 32 x 32 (NB = 1 or 2); v_mfma_f32_32x32x64_f8f6f4 with 4-bit (e2m1)
+// has NB x NB blocks of 32 x 32 (NB = 1, 2 or 4); v_mfma_f32_32x32x64_f8f6f4 with 4-bit (e2m1)
 // operands adds the products of 64 tokens per instruction, so 64 token-layers cost NB (NB + 1) / 2
-// matrix instructions (the blocks on and above the diagonal), whatever k is.
+// matrix instructions (the blocks on and above the diagonal: 3 at E <= 64, 10 at E <= 128),
+// whatever k is.
 //
 // Kernel design (gfx950): one wave per workgroup; W waves each take one contiguous range of the
 // flattened token-layers x = l * N + t (the split of the histogram kernel, so the partial slots and
@@ -12,13 +13,14 @@
 // Per batch of 64 token-layers (one per lane):
 //   * each lane forms its token's one-hot row in registers: a 64-bit mask of its ids (which also
 //     validates them: a repeated id leaves fewer than k bits, an id of E or more sets a bit outside
-//     the lane's valid set or a bit above bit 5 of its raw word), turned into one e2m1 nibble per
+//     the lane's valid set or a bit above bit 5 (bit 6 at NB = 4) of its raw word; at NB = 4 bit 6
+//     of the id picks the 64-bit half of the 128-bit mask), turned into one e2m1 nibble per
 //     expert (0x1 = 0.5, so a product is 0.25 and every float32 partial sum is exact).  The nibbles
 //     come from byte permutes used as a four-entry table: selector byte j = two mask bits, output
 //     byte j = those two bits as two nibbles, so a row of 32 experts costs four permutes, four ANDs
 //     and three shifts.  For that, row position n holds the mask bit relabel(n), where relabel
-//     swaps bit fields 4:3 and 2:1 of the 6-bit index (an involution that keeps bit 5, so both
-//     32-expert blocks keep their experts); the Gram matrix is thus counted over relabelled experts
+//     swaps bit fields 4:3 and 2:1 of the index (an involution that keeps bits 5 and 6, so every
+//     32-expert block keeps its experts); the Gram matrix is thus counted over relabelled experts
 //     and mapped back when the triangle is written;
 //   * the lane stores the row (16 NB bytes, token-major) into a wave-private LDS tile with 16-byte
 //     writes.  The 8-byte chunks of a row (16 experts each) sit at positions permuted by the row
@@ -70,8 +72,15 @@ __device__ __forceinline__ uint32_t tri_bin(uint32_t m, uint32_t n, uint32_t E) 
 // row and column positions are relabelled experts.
 // Expert index <-> row position (see the file comment): swap bits 4:3 with bits 2:1.
 __device__ __forceinline__ uint32_t relabel(uint32_t x) {
-  return (x & 0x21u) | ((x & 0x18u) >> 2) | ((x & 0x06u) << 2);
+  return (x & 0x61u) | ((x & 0x18u) >> 2) | ((x & 0x06u) << 2);
 }
+
+// Mask-bit permutations that XOR-ing the bit index with 4, 32 or 64 applies to a 128-bit mask held
+// as two 64-bit halves.
+__device__ __forceinline__ uint64_t swap_nibbles(uint64_t x) {
+  return ((x & 0x0f0f0f0f0f0f0f0full) << 4) | ((x >> 4) & 0x0f0f0f0f0f0f0f0full);
+}
+__device__ __forceinline__ uint64_t swap_dwords(uint64_t x) { return (x << 32) | (x >> 32); }
 
 __device__ __forceinline__ void store_block(const v16f& acc, int bi, int bj, int lane, uint32_t E,
                                             uint32_t* __restrict__ dst) {
@@ -137,11 +146,14 @@ __device__ __forceinline__ void mfma_blocks(const v4i (&frag)[NB], v16f (&acc)[N
 
 constexpr int log2i(int x) { return x <= 1 ? 0 : 1 + log2i(x / 2); }
 
-// NB = number of 32-expert blocks (1: E <= 32, 2: E <= 64).  The register budget is set for four
-// waves per SIMD (the three accumulator blocks take 48 registers).
+// NB = number of 32-expert blocks (1: E <= 32, 2: E <= 64, 4: E <= 128).  The register budget is set
+// for four waves per SIMD (the three accumulator blocks of NB = 2 take 48 registers), two at NB = 4
+// (ten blocks, 160 registers).
 template <int K, int NB>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void coact_mfma_kernel(MfmaArgs a) {
-  static_assert(NB == 1 || NB == 2, "one or two 32-expert blocks");
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(NB == 4 ? 2 : 4, 8))) void coact_mfma_kernel(
+    MfmaArgs a) {
+  static_assert(NB == 1 || NB == 2 || NB == 4, "one, two or four 32-expert blocks");
+  constexpr int kMaskWords = NB == 4 ? 4 : 2;  // 32-bit words of the id mask (ids below 32 kMaskWords)
   constexpr int kRowBytes = 16 * NB;                 // 4-bit one-hot row of 32 NB experts
   constexpr int kChunks = 2 * NB;                    // 8-byte chunks (16 experts) per row
   constexpr int kSwShift = log2i(128 / kRowBytes);   // s(j) = (j >> kSwShift) & (kChunks - 1)
@@ -163,11 +175,31 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
   const uint32_t sw_row = (static_cast<uint32_t>(lane) >> kSwShift) & (kChunks - 1);
   const uint32_t part_row = (static_cast<uint32_t>(lane) >> kPartShift) & (NB - 1);
   const uint32_t id_xor = relabel((sw_row ^ (part_row << 1)) << 4);
-  // mask bits b whose expert b ^ id_xor is >= E (E <= 64; id_xor has bits 2 and 5 only)
-  uint64_t nv = E >= 64u ? 0ull : (~0ull << E);
-  if (id_xor & 4u) nv = ((nv & 0x0f0f0f0f0f0f0f0full) << 4) | ((nv >> 4) & 0x0f0f0f0f0f0f0f0full);
-  if (id_xor & 32u) nv = (nv << 32) | (nv >> 32);
-  const uint32_t nv_lo = static_cast<uint32_t>(nv), nv_hi = static_cast<uint32_t>(nv >> 32);
+  // mask bits b whose expert b ^ id_xor is >= E (id_xor has bits 2, 5 and 6 only)
+  uint32_t nv[kMaskWords];
+  {
+    uint64_t lo = E >= 64u ? 0ull : (~0ull << E);
+    uint64_t hi = E >= 128u ? 0ull : (E <= 64u ? ~0ull : (~0ull << (E - 64u)));
+    if (id_xor & 4u) {
+      lo = swap_nibbles(lo);
+      hi = swap_nibbles(hi);
+    }
+    if (id_xor & 32u) {
+      lo = swap_dwords(lo);
+      hi = swap_dwords(hi);
+    }
+    if (id_xor & 64u) {
+      const uint64_t t = lo;
+      lo = hi;
+      hi = t;
+    }
+    nv[0] = static_cast<uint32_t>(lo);
+    nv[1] = static_cast<uint32_t>(lo >> 32);
+    if constexpr (kMaskWords == 4) {
+      nv[2] = static_cast<uint32_t>(hi);
+      nv[3] = static_cast<uint32_t>(hi >> 32);
+    }
+  }
   const uint32_t row_off = static_cast<uint32_t>(lane) * kRowBytes;
   // transposed reads: lane l = 16 g + i reads, for block b and half r, the chunk of experts
   // 32 b + 16 (g & 1) .. + 15 of row j = 32 (g >> 1) + 16 r + i
@@ -220,14 +252,41 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
 #pragma unroll
       for (int d = 0; d < kDepth; ++d) {
         const uint32_t base = rb + 64u * d;  // batch-uniform
-        // one-hot mask of the ids (the 64-bit shift uses the low six bits of its amount)
-        uint64_t m = 0;
+        // one-hot mask of the ids (the 64-bit shift uses the low six bits of its amount; at NB = 4
+        // bit 6 picks the 64-bit half)
+        uint32_t mw[kMaskWords];
+        if constexpr (kMaskWords == 2) {
+          uint64_t m = 0;
 #pragma unroll
-        for (int s = 0; s < K; ++s) m |= 1ull << (ring[d].id(s) ^ id_xor);
-        const uint32_t m_lo = static_cast<uint32_t>(m), m_hi = static_cast<uint32_t>(m >> 32);
+          for (int s = 0; s < K; ++s) m |= 1ull << ((ring[d].id(s) ^ id_xor) & 63u);
+          mw[0] = static_cast<uint32_t>(m);
+          mw[1] = static_cast<uint32_t>(m >> 32);
+        } else {
+#pragma unroll
+          for (int i = 0; i < kMaskWords; ++i) mw[i] = 0u;
+#pragma unroll
+          for (int s = 0; s < K; ++s) {
+            const uint32_t b = ring[d].id(s) ^ id_xor;
+            const uint64_t t = 1ull << (b & 63u);
+            const uint32_t t0 = static_cast<uint32_t>(t), t1 = static_cast<uint32_t>(t >> 32);
+            const uint32_t hs = static_cast<uint32_t>(__builtin_amdgcn_sbfe(static_cast<int>(b), 6, 1));
+            mw[0] = __builtin_amdgcn_bitop3_b32(mw[0], t0, hs, 0xF4);  // mw | (t & ~hs)
+            mw[1] = __builtin_amdgcn_bitop3_b32(mw[1], t1, hs, 0xF4);
+            mw[2] = __builtin_amdgcn_bitop3_b32(mw[2], t0, hs, 0xF8);  // mw | (t & hs)
+            mw[3] = __builtin_amdgcn_bitop3_b32(mw[3], t1, hs, 0xF8);
+          }
+        }
         const bool in_seg = lane < static_cast<int>(n - base);
-        const bool range_bad = ((ring[d].any_id_bits() & 0xffc0ffc0u) | (m_lo & nv_lo) | (m_hi & nv_hi)) != 0u;
-        const bool dup = __popc(m_lo) + __popc(m_hi) != K;
+        // raw ids of 64 (128 at NB = 4) or more, then mask bits of experts >= E
+        uint32_t oor = ring[d].any_id_bits() & (NB == 4 ? 0xff80ff80u : 0xffc0ffc0u);
+        int pop = 0;
+#pragma unroll
+        for (int i = 0; i < kMaskWords; ++i) {
+          oor |= mw[i] & nv[i];
+          pop += __popc(mw[i]);
+        }
+        const bool range_bad = oor != 0u;
+        const bool dup = pop != K;
         err |= (in_seg && range_bad) ? TACG_ERR_ID_RANGE : 0u;
         err |= (in_seg && !range_bad && dup) ? TACG_ERR_ID_DUP : 0u;
         // an invalid token-layer is flagged and not counted
@@ -240,7 +299,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
           uint8_t* rowp = tile + kBuf + row_off;
 #pragma unroll
           for (int q = 0; q < NB; ++q) {  // register part q (32 experts) to the row's part q ^ g(j)
-            const uint32_t src = q == 0 ? m_lo : m_hi;
+            const uint32_t src = mw[q];
             u32x4 v;
             v.x = nibble_pairs(src, keep);
             v.y = nibble_pairs(src >> 2, keep);
@@ -293,7 +352,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(4, 8))) void
 template <int K>
 void launch_k(const MfmaArgs& a, hipStream_t stream) {
   if (a.E <= 32) hipLaunchKernelGGL((coact_mfma_kernel<K, 1>), dim3(a.W), dim3(64), 0, stream, a);
-  else hipLaunchKernelGGL((coact_mfma_kernel<K, 2>), dim3(a.W), dim3(64), 0, stream, a);
+  else if (a.E <= 64) hipLaunchKernelGGL((coact_mfma_kernel<K, 2>), dim3(a.W), dim3(64), 0, stream, a);
+  else hipLaunchKernelGGL((coact_mfma_kernel<K, 4>), dim3(a.W), dim3(64), 0, stream, a);
 }
 
 }  // namespace
@@ -301,22 +361,30 @@ void launch_k(const MfmaArgs& a, hipStream_t stream) {
 // The matrix path costs about the same at any k, the histogram k (k - 1) / 2 LDS increments per
 // token-layer (coact.hip).  Measured on MI355X (kernel averages): at E = 64, top-6 (2^21 tokens x 27
 // layers) 143 us against 0.37 ms for the histogram; at E = 60, top-4 (2^22 tokens x 24 layers) 164 us
-// against 184 us.  At E = 128, top-8 the four-block variant of this kernel (ten products per 64
-// token-layers, 160 accumulator registers, two waves per SIMD) took 1.60 ms against the histogram's
-// 1.47 ms, so only E <= 64 uses it.
-bool coact_uses_mfma(int32_t n_experts, int32_t top_k) { return n_experts <= 64 && top_k >= 4; }
+// against 184 us.  The four-block kernel (E <= 128; ten products per 64 token-layers, 160 accumulator
+// registers, two waves per SIMD) costs twice the two-block one per token-layer, so it pays only from
+// top-8, timed per call on 2^21 tokens x 24 layers at E = 128: 0.365 against 0.376 ms at top-8 with
+// uniform ids, 0.384 against 0.305 ms at top-7, 0.349 against 0.244 ms at top-6; on the clustered
+// E = 128, top-8 trace of 2^22 tokens x 48 layers 1.18 against 1.43 ms.  Above top-12 its register
+// budget spills, so the histogram keeps those.
+bool coact_uses_mfma(int32_t n_experts, int32_t top_k) {
+  return (n_experts <= 64 && top_k >= 4) || (n_experts <= 128 && top_k >= 8 && top_k <= 12);
+}
 
-int coact_mfma_workgroups(int64_t total) {
-  // one wave per workgroup; about 8192 token-layers each, at most 4096 waves (16 per CU, all resident)
+int coact_mfma_workgroups(int64_t total, int32_t n_experts) {
+  // one wave per workgroup; about 8192 token-layers each, at most 16 waves per CU at E <= 64 and 8
+  // at E <= 128 (all resident)
+  const int64_t cap = n_experts <= 64 ? 4096 : 2048;
   const int64_t want = (total + 8191) / 8192;
-  return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(4096, want)));
+  return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(cap, want)));
 }
 
 int launch_coact_mfma_hist(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
                            int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam, int32_t W, int32_t nbins,
                            uint32_t* partial, uint32_t* d_err, hipStream_t stream) {
   // each wave addresses its range with 24-bit products of token-layer offsets: keep it below 2^24
-  // token-layers (at most 4096 waves, so this holds for any trace below 2^36 token-layers)
+  // token-layers (at least 2048 waves when the range is long, so this holds for any trace below 2^35
+  // token-layers)
   if ((n_tokens * n_layers + W - 1) / W >= (int64_t(1) << 24)) return TACG_E_UNSUPPORTED;
   MfmaArgs a{};
   a.trace = trace;

@@ -38,7 +38,7 @@ int coact_num_workgroups(int64_t total_token_layers, int32_t n_experts, int32_t 
 size_t coact_bins(int32_t n_experts, int32_t top_k);
 // small expert counts: the counts come from int8 matrix products (coact_mfma.hip)
 bool coact_uses_mfma(int32_t n_experts, int32_t top_k);
-int coact_mfma_workgroups(int64_t total_token_layers);
+int coact_mfma_workgroups(int64_t total_token_layers, int32_t n_experts);
 int launch_coact_mfma_hist(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
                            int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam, int32_t W, int32_t nbins,
                            uint32_t* partial, uint32_t* d_err, hipStream_t stream);

@@ -33,6 +33,18 @@ def test_exports_every_declared_symbol(L):
         assert hasattr(L, n), n
 
 
+def test_coact_kernel_choice(L):
+    """The co-activation build's kernel choice (a host-only query): matrix cores at E <= 64 from top-4,
+    at E <= 128 for top-8 to top-12, the LDS histogram otherwise; 0 for shapes the build rejects."""
+    use = L.tacg_coact_uses_matrix_cores
+    assert [use(64, k) for k in (1, 2, 3, 4, 6, 16)] == [0, 0, 0, 1, 1, 1]
+    assert [use(32, k) for k in (3, 4, 12)] == [0, 1, 1]
+    assert [use(128, k) for k in (4, 6, 7, 8, 10, 12, 13, 16)] == [0, 0, 0, 1, 1, 1, 0, 0]
+    assert [use(65, 8), use(129, 8), use(256, 8), use(256, 4)] == [1, 0, 0, 0]
+    assert [use(0, 4), use(64, 0), use(64, 17), use(4, 6), use(257, 8), use(-1, 8)] == [0] * 6
+    assert tacg.coact_uses_matrix_cores(60, 4) and not tacg.coact_uses_matrix_cores(256, 8)
+
+
 def test_strerror(L):
     for code in (0, -1, -2, -3, 7):
         assert isinstance(L.tacg_strerror(code), bytes)

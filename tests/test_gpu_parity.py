@@ -81,6 +81,12 @@ def _rand_trace(L, N, k, E, seed, device="cuda"):
     (64, 4, 2, [4000, 900, 3], 23),
     (32, 4, 3, [2500, 0, 1200], 24),
     (20, 4, 2, [3100, 77], 25),
+    # the four-block matrix path (64 < E <= 128, 8 <= k <= 12) and the histogram around it
+    (100, 8, 2, [3000, 1, 2200], 26),
+    (65, 12, 1, [2600, 900], 27),
+    (128, 7, 2, [3000, 2000], 28),
+    (128, 13, 1, [2500], 29),
+    (97, 6, 2, [3500, 1500], 30),
 ])
 def test_coact_parity(E, k, L, counts, seed):
     _say(f"coact E={E} k={k} L={L} counts={counts}")
@@ -155,7 +161,8 @@ def test_coact_repeated_builds_exact(E, k, counts, L):
     assert _err(err) == 0
 
 
-@pytest.mark.parametrize("E,k", [(16, 4), (16, 6), (200, 8), (64, 8), (32, 5)])   # histogram / matrix-core paths
+@pytest.mark.parametrize("E,k", [(16, 4), (16, 6), (200, 8), (64, 8), (32, 5), (100, 7), (128, 12), (96, 9),
+                                 (256, 6), (200, 7)])   # histogram / matrix-core paths
 def test_coact_data_errors_flagged(E, k):
     """Repeated and out-of-range ids are flagged; the offending token-layer is skipped, as the oracle
     skips it."""

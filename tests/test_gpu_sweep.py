@@ -4,9 +4,9 @@ grouping objective) against the oracle on the same inputs.
 
 The shapes are drawn to reach the kernels' branches in combination: expert counts on both sides of
 the 64 / 128 launch thresholds, every top-k width from 1 to 16 (packed ids of one to four words, the
-matrix-core path at E <= 64 and k >= 4), one to five small families with empty ones, 1 to 32 GPUs
-with narrow and wide bands, zero to four secondaries with up to 16 replicated experts, the guard on
-and off, and decay factors 0, 0.5 and 0.995.  A large-shape variant draws up to eight families of up
+matrix-core paths at E <= 64 from k = 4 and at E <= 128 for k = 8 to 12), one to five small families
+with empty ones, 1 to 32 GPUs with narrow and wide bands, zero to four secondaries with up to 16
+replicated experts, the guard on and off, and decay factors 0, 0.5 and 0.995.  A large-shape variant draws up to eight families of up
 to 60,000 tokens (some nearly empty), so that several co-activation workgroups meet at segment
 boundaries and the scoring kernel runs many pieces.  Counts, costs, loads and the final float64
 loads are compared exactly; float outputs within the tolerances of the other parity tests.
