@@ -109,9 +109,9 @@ def test_coact_tiny_config():
     np.testing.assert_array_equal(_u32(C), Co)
 
 
-def test_coact_accumulate_chunks():
+@pytest.mark.parametrize("E,k", [(64, 6), (128, 8), (256, 8), (100, 5)])  # both matrix paths, histograms
+def test_coact_accumulate_chunks(E, k):
     """Streaming: counting a trace in two token chunks with TACG_ACCUMULATE equals one call."""
-    E, k = 64, 6
     counts = [6000, 4000]
     off = synth.fam_offsets(counts)
     tr = _rand_trace(2, 10000, k, E, 11)
@@ -178,7 +178,7 @@ def test_coact_data_errors_flagged(E, k):
         np.testing.assert_array_equal(_u32(D), Do)
 
 
-@pytest.mark.parametrize("E,k", [(16, 4), (16, 6), (64, 8)])
+@pytest.mark.parametrize("E,k", [(16, 4), (16, 6), (64, 8), (100, 8), (256, 8)])
 def test_coact_empty_trace(E, k):
     tr = torch.zeros((2, 0, k), dtype=torch.int16, device="cuda")
     D, C, err = tacg.coact_build(tr, [0, 0, 0], E)
