@@ -1,4 +1,4 @@
-// Co-activation counts of small expert counts (E <= 64) on the matrix cores.
+// Co-activation counts of small expert counts (E <= 128) on the matrix cores.
 //
 // For the tokens of one (family, layer) segment, C = R^T R where R[t][e] = 1 when token t selected
 // expert e (Sec. 3.3: C counts the tokens that chose both experts).  With E <= 32 NB the Gram matrix
@@ -11,11 +11,11 @@
 // flattened token-layers x = l * N + t (the split of the histogram kernel, so the partial slots and
 // the reduction are shared).  The ids of the next four batches are in flight while one is counted.
 // Per batch of 64 token-layers (one per lane):
-//   * each lane forms its token's one-hot row in registers: a 64-bit mask of its ids (which also
-//     validates them: a repeated id leaves fewer than k bits, an id of E or more sets a bit outside
-//     the lane's valid set or a bit above bit 5 (bit 6 at NB = 4) of its raw word; at NB = 4 bit 6
-//     of the id picks the 64-bit half of the 128-bit mask), turned into one e2m1 nibble per
-//     expert (0x1 = 0.5, so a product is 0.25 and every float32 partial sum is exact).  The nibbles
+//   * each lane forms its token's one-hot row in registers: a 64-bit mask of its ids (128-bit at
+//     NB = 4, where bit 6 of the id picks the 64-bit half), which also validates them: a repeated
+//     id leaves fewer than k bits, an id of E or more sets a bit outside the lane's valid set or a
+//     bit above bit 5 (bit 6 at NB = 4) of its raw word.  The mask is turned into one e2m1 nibble
+//     per expert (0x1 = 0.5, so a product is 0.25 and every float32 partial sum is exact).  The nibbles
 //     come from byte permutes used as a four-entry table: selector byte j = two mask bits, output
 //     byte j = those two bits as two nibbles, so a row of 32 experts costs four permutes, four ANDs
 //     and three shifts.  For that, row position n holds the mask bit relabel(n), where relabel
