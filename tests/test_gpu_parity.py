@@ -87,6 +87,9 @@ def _rand_trace(L, N, k, E, seed, device="cuda"):
     (128, 7, 2, [3000, 2000], 28),
     (128, 13, 1, [2500], 29),
     (97, 6, 2, [3500, 1500], 30),
+    # top-6 and top-7 histograms (the lane orders through constant lane masks) at E > 128
+    (256, 6, 2, [20000, 30000], 31),
+    (160, 7, 2, [15000, 1, 9000], 32),
 ])
 def test_coact_parity(E, k, L, counts, seed):
     _say(f"coact E={E} k={k} L={L} counts={counts}")
