@@ -193,8 +193,8 @@ __device__ __forceinline__ void count_token(const RawIds<K>& raw, bool valid, ui
           }
         } else {
           // At top-6 and top-7 the plain selects above were turned into selects of array indices
-          // and then into chains of selects (about 220 and 430 VALU instructions per token-layer
-          // instead of about 36 and 48; 2.5x and 3.5x slower at E = 256).  Here the selects take
+          // and then into chains of selects (about 220 and 430 select instructions per token-layer
+          // instead of 36 and 48; 2.5x and 3.5x slower at E = 256).  Here the selects take
           // their lane masks from constant SGPR pairs, two per pair.  At top-8 the compiler keeps
           // two selects per pair by itself, and its schedule measured 0.7 % faster.
           uint32_t x[NP];
