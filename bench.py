@@ -33,14 +33,24 @@ CALIB_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
 
 
+def code_text(src: str) -> str:
+    """The code of a C/C++/HIP source without its comments and layout (comments become one space,
+    runs of white space one space)."""
+    import re
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
 def source_digest(files) -> str:
-    """SHA-256 over the HIP sources that hold one kernel (and the shared internal header): HBM
-    traffic figures are only reported for the kernel code they were measured on."""
+    """SHA-256 over the code of the HIP sources that hold one kernel (and the shared internal header),
+    comments and layout left out: HBM traffic figures are only reported for the kernel code they
+    were measured on."""
     import hashlib
     h = hashlib.sha256()
     for f in sorted(set(files) | {"tacg_internal.h"}):
         h.update(f.encode())
-        h.update(open(os.path.join(ROOT, "paper_2606_01007_amd", "csrc", f), "rb").read())
+        h.update(code_text(open(os.path.join(ROOT, "paper_2606_01007_amd", "csrc", f)).read()).encode())
     return h.hexdigest()
 
 

@@ -58,6 +58,14 @@ def test_traffic_from_counter_files(tmp_path, monkeypatch):
     assert bench.measured_traffic("ev_main", "deepseek_v3") is None
 
 
+def test_source_digest_follows_code_not_comments():
+    """The traffic record's source digest changes with the code and not with comments or layout."""
+    a = "int f(int x) {  // doubles\n  return 2 * x; /* a\n block */ }\n"
+    assert bench.code_text(a) == bench.code_text("int f(int x) {\n\n return 2 * x; }")
+    assert bench.code_text(a) != bench.code_text("int f(int x) { return 3 * x; }")
+    assert bench.code_text("a = b; // x\nc = d;") == "a = b; c = d;"
+
+
 def test_traffic_needs_the_calibration_copy(tmp_path, monkeypatch):
     monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "hbm_traffic.json"))
     fetch, write = tmp_path / "f.csv", tmp_path / "w.csv"
