@@ -173,7 +173,9 @@ int tacg_placement_load(const uint32_t* D, int32_t n_fam, int32_t n_layers, int3
  * load_ref[P][L][G] (required when n_sec > 0; see tacg_placement_load).  Host arrays home_start_host
  * and home_size_host [F] must satisfy home_size >= 1 and home_start + home_size <= G.
  * theta_num and theta_den lie in 0 .. 2^20 (theta_num is not read when theta_den == 0).
- * Data errors: TACG_ERR_ID_RANGE / _DUP (trace), TACG_ERR_TABLE, TACG_ERR_LIMIT.
+ * Data errors: TACG_ERR_ID_RANGE / _DUP (trace: the offending token-layer is not scored, so it adds
+ * to no cost, load or count, and the sums above run over the valid token-layers), TACG_ERR_TABLE,
+ * TACG_ERR_LIMIT.
  * workspace: tacg_eval_workspace_bytes(...) bytes.  flags: must be 0.
  */
 int tacg_eval_placements(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,

@@ -55,6 +55,7 @@ struct EvWs {
   unsigned long long* acc_span_fam;   // [F][P] sum of |cards| over the family's token-layers
   unsigned long long* acc_cross_fam;  // [F][P] token-layers whose cards span several bands
   unsigned long long* acc_hmass_fam;  // [F][P] replicated-slot dispatches served in the family's band
+  unsigned long long* n_bad;          // [1] token-layers not scored: an id out of range or repeated
 };
 
 __host__ __device__ inline int32_t even_up(int32_t P) { return P + (P & 1); }
@@ -76,6 +77,7 @@ EvWs carve_ev(void* ws, int32_t L, int32_t E, int32_t G, int32_t P, int32_t F, s
   r.acc_span_fam = c.take<unsigned long long>(static_cast<size_t>(P) * F);
   r.acc_cross_fam = c.take<unsigned long long>(static_cast<size_t>(P) * F);
   r.acc_hmass_fam = c.take<unsigned long long>(static_cast<size_t>(P) * F);
+  r.n_bad = c.take<unsigned long long>(1);
   if (used) *used = c.used;
   return r;
 }
@@ -117,6 +119,7 @@ __global__ __launch_bounds__(256) void ev_zero(EvArgs a) {
   }
   for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.F; j += stride) w.acc_fam[j] = 0;
   for (int64_t j = i; j < static_cast<int64_t>(even_up(a.P)) * a.L * a.G; j += stride) w.rep_load[j] = 0;
+  if (i == 0) *w.n_bad = 0;
   if (a.stats) {
     for (int64_t j = i; j < static_cast<int64_t>(a.F) * a.L * a.E; j += stride) w.cnt_fam[j] = 0;
     for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.F; j += stride) {
@@ -277,6 +280,7 @@ struct InfoLayout {
   static constexpr int kHomeShift = kMaskBits;
   static constexpr int kRepShift = kMaskBits + 5;
   static constexpr int kRepSlots = K <= 8 ? 4 : 2;
+  static constexpr uint32_t kBad = 1u << 31;  // the token-layer is not scored (invalid ids)
 };
 
 // Index of the lowest set bit, 0xffffffff for 0 (the hardware v_ffbl_b32 result).
@@ -418,6 +422,7 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
   const int E = a.E, G = a.G, L = a.L;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  uint32_t n_bad = 0;  // invalid token-layers met by this wave (wave-uniform)
   const int nwaves = blockDim.x >> 6;
   const int16_t* trace_l = a.trace + static_cast<int64_t>(l) * a.N * K;
   S sc;
@@ -441,6 +446,7 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
 #pragma unroll
       for (int w = 0; w < KB; ++w) pk[w] = 0;
       uint32_t info = 0;
+      bool bad = false;
       if (t < r_end) {
         const int16_t* idp = trace_l + static_cast<int64_t>(t) * K;
         uint32_t raw[K];
@@ -461,15 +467,18 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
           pk[s >> 2] |= id << (8 * (s & 3));
         }
         info |= ((t - off_f) % hz) << IL::kHomeShift;
+        bool dup = false;
+#pragma unroll
+        for (int s = 1; s < K; ++s)
+#pragma unroll
+          for (int q = 0; q < s; ++q) dup |= raw[s] == raw[q];
+        // an invalid token-layer is flagged and not scored (its ids stay clamped in range, unused)
+        bad = !ok || dup;
+        if (bad) info = IL::kBad;
         if (counter) {
-          bool dup = false;
-#pragma unroll
-          for (int s = 1; s < K; ++s)
-#pragma unroll
-            for (int q = 0; q < s; ++q) dup |= raw[s] == raw[q];
           if (!ok) err |= TACG_ERR_ID_RANGE;
           if (dup) err |= TACG_ERR_ID_DUP;
-          if (ok && !dup) {
+          if (!bad) {
 #pragma unroll
             for (int s = 0; s < K; ++s)
               __hip_atomic_fetch_add(&ecnt[raw[s]], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
@@ -477,30 +486,36 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
         }
       }
       const uint32_t ntile = min(64u, r_end - tile);
-      n_scored += ntile;
+      const uint32_t nbad = static_cast<uint32_t>(__builtin_popcountll(__builtin_amdgcn_ballot_w64(bad)));
+      n_scored += ntile - nbad;
+      n_bad += nbad;
       uint32_t j = 0;
-      for (; j + U <= ntile; j += U) {
-        uint32_t ids[U][KB], tinfo[U];
+      if (nbad == 0u) {  // wave-uniform: a tile with invalid token-layers takes the loop below
+        for (; j + U <= ntile; j += U) {
+          uint32_t ids[U][KB], tinfo[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
+          for (int u = 0; u < U; ++u) {
 #pragma unroll
-          for (int w = 0; w < KB; ++w) ids[u][w] = __builtin_amdgcn_readlane(pk[w], j + u);
-          tinfo[u] = __builtin_amdgcn_readlane(info, j + u);
-        }
-        uint32_t m[U][PPL];
+            for (int w = 0; w < KB; ++w) ids[u][w] = __builtin_amdgcn_readlane(pk[w], j + u);
+            tinfo[u] = __builtin_amdgcn_readlane(info, j + u);
+          }
+          uint32_t m[U][PPL];
 #pragma unroll
-        for (int u = 0; u < U; ++u) sc.gather(ids[u], m[u]);
+          for (int u = 0; u < U; ++u) sc.gather(ids[u], m[u]);
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-          sc.resolve(tinfo[u], ids[u], m[u]);
-          sc.account(tinfo[u], m[u]);
+          for (int u = 0; u < U; ++u) {
+            sc.resolve(tinfo[u], ids[u], m[u]);
+            sc.account(tinfo[u], m[u]);
+          }
         }
       }
+      // the tile's last token-layers, or all of a tile with invalid ones, one at a time
       for (; j < ntile; ++j) {
         uint32_t ids[KB];
 #pragma unroll
         for (int w = 0; w < KB; ++w) ids[w] = __builtin_amdgcn_readlane(pk[w], j);
         const uint32_t tinfo = __builtin_amdgcn_readlane(info, j);
+        if (tinfo & IL::kBad) continue;
         uint32_t m[PPL];
         sc.gather(ids, m);
         sc.resolve(tinfo, ids, m);
@@ -522,6 +537,8 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
       __syncthreads();
     }
   }
+  // the workgroups of placement block 0 see every token-layer once: they count the invalid ones
+  if (counter && n_bad != 0u && lane == 0) atomicAdd(a.ws.n_bad, static_cast<unsigned long long>(n_bad));
   if (nrep > 0) {  // one global add per counter and workgroup
 #pragma unroll
     for (int c = 0; c < kRcntPerThread; ++c) {
@@ -706,7 +723,8 @@ __global__ __launch_bounds__(256) void ev_finalize(EvArgs a, uint64_t* __restric
   if (l == 0) {
     if (threadIdx.x == 0) {
       cost_home[p] = a.ws.acc_home[p];
-      cost_span[p] = a.ws.acc_span[p] - static_cast<uint64_t>(a.N) * static_cast<uint64_t>(L);
+      // |cards| - 1 per scored token-layer (every scored token-layer has at least one card)
+      cost_span[p] = a.ws.acc_span[p] - (static_cast<uint64_t>(a.N) * static_cast<uint64_t>(L) - *a.ws.n_bad);
     }
     if (cost_home_fam)
       for (int f = threadIdx.x; f < a.F; f += blockDim.x)

@@ -39,14 +39,14 @@ def _rand_trace(L, N, k, E, seed):
     return torch.topk(x, k, dim=2).indices.to(torch.int16)
 
 
-def _both(tr, off, E, hs, hz, G, prim, sec, rho, theta, state=None):
+def _both(tr, off, E, hs, hz, G, prim, sec, rho, theta, state=None, expect_err=0):
     ro = oracle.score_online(tr, off, E, hs, hz, G, prim, sec, rho=rho, theta=theta, state=state)
-    assert ro["err"] == 0
+    assert ro["err"] == expect_err
     st = torch.as_tensor(state).cuda() if state is not None else None
     out = tacg.eval_online(tr.cuda() if isinstance(tr, torch.Tensor) else torch.as_tensor(tr).cuda(), off, E, hs, hz,
                            G, torch.as_tensor(prim).cuda(),
                            torch.as_tensor(sec).cuda() if sec is not None else None, rho=rho, theta=theta, state=st)
-    assert _err(out["err"]) == 0
+    assert _err(out["err"]) == expect_err
     np.testing.assert_array_equal(out["cost_home"].cpu().numpy(), ro["cost_home"])
     np.testing.assert_array_equal(out["cost_span"].cpu().numpy(), ro["cost_span"])
     np.testing.assert_array_equal(tacg.as_u32(out["load"]).cpu().numpy(), ro["load"])
@@ -122,6 +122,23 @@ def test_online_state_carry_and_initial_state():
                                     cost_home_fam=None, state=st))
     torch.cuda.synchronize()
     np.testing.assert_array_equal(st.cpu().numpy(), whole["state"].cpu().numpy())
+
+
+def test_online_invalid_ids_not_served():
+    """Token-layers with an id out of range or a repeated id are flagged, not served and leave the
+    decayed loads untouched, as in the oracle: every output, the final loads included, is equal."""
+    cfg = synth.CONFIGS["deepseek_v3"]
+    w = synth.make_workload("deepseek_v3", n_tokens=16 * 300 + 11, layers=2, n_place=70)
+    ps = w.placement_sets[0]
+    tr = w.trace_serve.clone()
+    L, N, k = tr.shape
+    rng = np.random.default_rng(31)
+    for i in range(24):
+        l, t, s = int(rng.integers(L)), int(rng.integers(N)), int(rng.integers(k))
+        tr[l, t, s] = [cfg.E, -2, int(tr[l, t, (s + 1) % k])][i % 3]
+    _say("online invalid ids")
+    _both(tr, w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], ps["n_gpus"], ps["primary"],
+          ps["secondary"], 0.995, (3, 20), expect_err=tacg.ERR_ID_RANGE | tacg.ERR_ID_DUP)
 
 
 def test_online_errors_flagged():

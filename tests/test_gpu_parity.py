@@ -235,11 +235,11 @@ def test_reweight_empty_family_and_zero_layer():
 # ------------------------------------------------------------------------------------------------
 # placement scoring
 # ------------------------------------------------------------------------------------------------
-def _score_both(w, ps, E, theta=(3, 20), use_oracle_ref=False):
+def _score_both(w, ps, E, theta=(3, 20), use_oracle_ref=False, tr=None, expect_err=0):
     G = ps["n_gpus"]
     prim = torch.as_tensor(ps["primary"]).cuda()
     sec = torch.as_tensor(ps["secondary"]).cuda() if ps["secondary"] is not None else None
-    tr = w.trace_serve
+    tr = w.trace_serve if tr is None else tr
     Do, _, _ = oracle.coact(tr.cpu(), w.fam_off_serve, E)
     ref_o = oracle.placement_load(Do, ps["primary"], G) if sec is not None else None
     ref_g = None
@@ -249,13 +249,13 @@ def _score_both(w, ps, E, theta=(3, 20), use_oracle_ref=False):
         else:
             D, _, e1 = tacg.coact_build(tr, w.fam_off_serve, E)
             ref_g = tacg.placement_load(D, prim, G, err=e1)
-            assert _err(e1) == 0
+            assert _err(e1) == expect_err
     out = tacg.eval_placements(tr, w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, prim, sec, ref_g,
                                theta=theta)
-    assert _err(out["err"]) == 0
+    assert _err(out["err"]) == expect_err
     ro = oracle.score(tr.cpu(), w.fam_off_serve, E, ps["home_start"], ps["home_size"], G, ps["primary"],
                       ps["secondary"], ref_o, theta)
-    assert ro["err"] == 0
+    assert ro["err"] == expect_err
     if ref_g is not None:
         np.testing.assert_array_equal(ref_g.cpu().numpy(), ref_o)
     np.testing.assert_array_equal(out["cost_home"].cpu().numpy(), ro["cost_home"])
@@ -280,6 +280,41 @@ def test_eval_parity(name, setidx, n_place, theta):
     w = synth.make_workload(name, device="cuda", n_tokens=n, layers=min(cfg.L, 3), n_place=n_place)
     _say(f"eval {name} set{setidx} P={n_place} theta={theta}")
     _score_both(w, w.placement_sets[setidx], cfg.E, theta)
+
+
+def _plant_invalid(tr, E, seed):
+    """A copy of trace tr with invalid token-layers: ids out of range (E, negative), repeated ids, a
+    run of four invalid token-layers (one scoring group), one invalid token-layer among three valid
+    ones, and the trace's last token-layer."""
+    tr = tr.clone()
+    L, N, k = tr.shape
+    rng = np.random.default_rng(seed)
+    spots = [(int(rng.integers(L)), int(rng.integers(N))) for _ in range(40)]
+    spots += [(0, t) for t in range(64, 68)] + [(L - 1, 130), (L - 1, N - 1)]
+    for i, (l, t) in enumerate(spots):
+        s = int(rng.integers(k))
+        kind = i % 3
+        if kind == 0:
+            tr[l, t, s] = E
+        elif kind == 1:
+            tr[l, t, s] = -1 - int(rng.integers(100))
+        else:
+            tr[l, t, s] = tr[l, t, (s + 1) % k]
+    return tr
+
+
+@pytest.mark.parametrize("name,setidx,n_place", [("tiny", 0, 16), ("deepseek16b", 0, 130), ("qwen15", 0, 70),
+                                                 ("deepseek_v3", 0, 65)])
+def test_eval_invalid_ids_not_scored(name, setidx, n_place):
+    """A token-layer with an id out of range or a repeated id is flagged and not scored, as in the
+    oracle: every cost, load and per-family cost equals the oracle's on a trace with such token-layers
+    (the replicated-slot choices and the snapshot loads of the guard skip them too)."""
+    cfg = synth.CONFIGS[name]
+    n = cfg.tokens_group if name == "tiny" else cfg.F * 1500 + 37
+    w = synth.make_workload(name, device="cuda", n_tokens=n, layers=min(cfg.L, 3), n_place=n_place)
+    _say(f"eval invalid ids {name} P={n_place}")
+    tr = _plant_invalid(w.trace_serve, cfg.E, 17)
+    _score_both(w, w.placement_sets[setidx], cfg.E, tr=tr, expect_err=tacg.ERR_ID_RANGE | tacg.ERR_ID_DUP)
 
 
 @pytest.mark.parametrize("band", [1, 2, 4, 8])

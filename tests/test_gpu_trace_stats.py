@@ -38,7 +38,7 @@ def _rand_trace(L, N, k, E, seed):
     return torch.topk(x, k, dim=2).indices.to(torch.int16)
 
 
-def _both(tr, off, E, hs, hz, G, prim, sec=None, theta=(3, 20)):
+def _both(tr, off, E, hs, hz, G, prim, sec=None, theta=(3, 20), expect_err=0):
     """Device statistics vs the oracle's on the same trace and tables (loads for the guard from each
     side's own counting pass)."""
     tr_c = torch.as_tensor(tr).cpu()
@@ -47,7 +47,7 @@ def _both(tr, off, E, hs, hz, G, prim, sec=None, theta=(3, 20)):
         Do, _, _ = oracle.coact(tr_c, off, E)
         ref_o = oracle.placement_load(Do, prim, G)
     ro = oracle.score(tr_c, off, E, hs, hz, G, prim, sec, ref_o, theta, stats=True)
-    assert ro["err"] == 0
+    assert ro["err"] == expect_err
     tr_g = tr_c.cuda()
     prim_t = torch.as_tensor(prim).cuda()
     sec_t = torch.as_tensor(sec).cuda() if sec is not None else None
@@ -55,9 +55,9 @@ def _both(tr, off, E, hs, hz, G, prim, sec=None, theta=(3, 20)):
     if sec is not None:
         D, _, e1 = tacg.coact_build(tr_g, off, E)
         ref_g = tacg.placement_load(D, prim_t, G, err=e1)
-        assert _err(e1) == 0
+        assert _err(e1) == expect_err
     out = tacg.eval_trace_stats(tr_g, off, E, hs, hz, G, prim_t, sec_t, ref_g, theta=theta)
-    assert _err(out["err"]) == 0
+    assert _err(out["err"]) == expect_err
     for key in ("span_fam", "cross_fam", "home_mass_fam", "cost_home", "cost_span"):
         np.testing.assert_array_equal(out[key].cpu().numpy(), ro[key], err_msg=key)
     np.testing.assert_array_equal(tacg.as_u32(out["load"]).cpu().numpy(), ro["load"])
@@ -92,6 +92,25 @@ def test_trace_stats_presets(name, setidx, n_place):
     _say(f"trace stats {name} set{setidx} P={n_place}")
     _both(w.trace_serve, w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], ps["n_gpus"], ps["primary"],
           ps["secondary"])
+
+
+@pytest.mark.parametrize("name,n_place", [("deepseek16b", 130), ("deepseek_v3", 65)])
+def test_trace_stats_invalid_ids_not_counted(name, n_place):
+    """Token-layers with an id out of range or a repeated id are flagged and left out of every
+    statistic, cost and load, as in the oracle."""
+    cfg = synth.CONFIGS[name]
+    w = synth.make_workload(name, n_tokens=cfg.F * 900 + 37, layers=2, n_place=n_place)
+    ps = w.placement_sets[0]
+    tr = w.trace_serve.clone()
+    L, N, k = tr.shape
+    rng = np.random.default_rng(23)
+    for i in range(30):
+        l, t, s = int(rng.integers(L)), int(rng.integers(N)), int(rng.integers(k))
+        tr[l, t, s] = [cfg.E, -7, int(tr[l, t, (s + 1) % k])][i % 3]
+    tr[:, 64:68, 0] = cfg.E   # a whole group of four
+    _say(f"trace stats invalid ids {name}")
+    _both(tr, w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], ps["n_gpus"], ps["primary"],
+          ps["secondary"], expect_err=tacg.ERR_ID_RANGE | tacg.ERR_ID_DUP)
 
 
 @pytest.mark.parametrize("band", [2, 4, 8, 32])
