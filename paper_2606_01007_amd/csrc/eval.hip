@@ -9,7 +9,10 @@
 //   ev_repinfo   per (placement, layer, replicated expert): feasible candidate mask FC, the
 //                fallback GPU argmin_{m in FC} load_ref (ties: lowest number) and whether the expert
 //                has a single candidate in that placement
-//   ev_main      the trace pass (below); also counts every expert's dispatches and validates ids
+//   ev_valid     validate the trace's ids: flag and count the token-layers with an id out of range
+//                or a repeated id, and mark their groups of 64 token-layers
+//   ev_main      the trace pass (below); also counts every expert's dispatches; an invalid token-layer
+//                (checked again only in marked groups) is not scored
 //   ev_finalize  loads = counts of single-candidate experts on their primary + replicated choices;
 //                costs from the accumulators
 //
@@ -56,11 +59,15 @@ struct EvWs {
   unsigned long long* acc_cross_fam;  // [F][P] token-layers whose cards span several bands
   unsigned long long* acc_hmass_fam;  // [F][P] replicated-slot dispatches served in the family's band
   unsigned long long* n_bad;          // [1] token-layers not scored: an id out of range or repeated
+  uint32_t* bad_tiles;                // [ceil(N L / 64 / 32)] bit g: token-layers 64 g .. 64 g + 63 of
+                                      // the flattened trace (x = l N + t) hold an invalid one
 };
 
 __host__ __device__ inline int32_t even_up(int32_t P) { return P + (P & 1); }
 
-EvWs carve_ev(void* ws, int32_t L, int32_t E, int32_t G, int32_t P, int32_t F, size_t* used = nullptr) {
+__host__ __device__ inline int64_t bad_tile_words(int64_t N, int32_t L) { return (N * L + 2047) / 2048; }
+
+EvWs carve_ev(void* ws, int64_t N, int32_t L, int32_t E, int32_t G, int32_t P, int32_t F, size_t* used = nullptr) {
   Carver c{static_cast<char*>(ws), 0};
   EvWs r;
   r.cnt = c.take<uint32_t>(static_cast<size_t>(L) * E);
@@ -78,6 +85,7 @@ EvWs carve_ev(void* ws, int32_t L, int32_t E, int32_t G, int32_t P, int32_t F, s
   r.acc_cross_fam = c.take<unsigned long long>(static_cast<size_t>(P) * F);
   r.acc_hmass_fam = c.take<unsigned long long>(static_cast<size_t>(P) * F);
   r.n_bad = c.take<unsigned long long>(1);
+  r.bad_tiles = c.take<uint32_t>(static_cast<size_t>(bad_tile_words(N, L)));
   if (used) *used = c.used;
   return r;
 }
@@ -120,6 +128,7 @@ __global__ __launch_bounds__(256) void ev_zero(EvArgs a) {
   for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.F; j += stride) w.acc_fam[j] = 0;
   for (int64_t j = i; j < static_cast<int64_t>(even_up(a.P)) * a.L * a.G; j += stride) w.rep_load[j] = 0;
   if (i == 0) *w.n_bad = 0;
+  for (int64_t j = i; j < bad_tile_words(a.N, a.L); j += stride) w.bad_tiles[j] = 0;
   if (a.stats) {
     for (int64_t j = i; j < static_cast<int64_t>(a.F) * a.L * a.E; j += stride) w.cnt_fam[j] = 0;
     for (int64_t j = i; j < static_cast<int64_t>(a.P) * a.F; j += stride) {
@@ -128,6 +137,45 @@ __global__ __launch_bounds__(256) void ev_zero(EvArgs a) {
       w.acc_hmass_fam[j] = 0;
     }
   }
+}
+
+// Trace validation (a1): every token-layer's ids, one wave per 64 consecutive token-layers of the
+// flattened trace (x = l * N + t), grid-stride.  A token-layer with an id out of range or a repeated id
+// is flagged, counted (n_bad) and marks its group of 64 in bad_tiles, so that ev_main checks the ids
+// itself only in the few tiles that meet a marked group.
+template <int K>
+__global__ __launch_bounds__(256) void ev_valid(EvArgs a) {
+  const int64_t total = a.N * a.L;
+  const int lane = threadIdx.x & 63;
+  const int64_t nwaves = static_cast<int64_t>(gridDim.x) * (blockDim.x >> 6);
+  uint32_t err = 0;
+  for (int64_t g = static_cast<int64_t>(blockIdx.x) * (blockDim.x >> 6) + (threadIdx.x >> 6); g * 64 < total;
+       g += nwaves) {
+    const int64_t x = g * 64 + lane;
+    bool bad = false;
+    if (x < total) {
+      const int16_t* idp = a.trace + x * K;
+      uint32_t raw[K];
+#pragma unroll
+      for (int s = 0; s < K; ++s) raw[s] = static_cast<uint16_t>(idp[s]);
+      bool ok = true, dup = false;
+#pragma unroll
+      for (int s = 0; s < K; ++s) {
+        ok &= raw[s] < static_cast<uint32_t>(a.E);
+#pragma unroll
+        for (int q = 0; q < s; ++q) dup |= raw[s] == raw[q];
+      }
+      if (!ok) err |= TACG_ERR_ID_RANGE;
+      if (dup) err |= TACG_ERR_ID_DUP;
+      bad = !ok || dup;
+    }
+    const uint64_t b = __builtin_amdgcn_ballot_w64(bad);
+    if (b != 0u && lane == 0) {
+      atomicOr(&a.ws.bad_tiles[g >> 5], 1u << (g & 31));
+      atomicAdd(a.ws.n_bad, static_cast<unsigned long long>(__builtin_popcountll(b)));
+    }
+  }
+  if (err) atomicOr(a.d_err, err);
 }
 
 // Table validation and the replicated-expert marks.  Flat grid-stride loop over (p, l, e).
@@ -401,11 +449,11 @@ struct Scorer {
 
 // Token loop of one workgroup (see ev_main).  NARROW: the family's band has at most 4 GPUs, so the
 // fallback choices are packed per band position.
-template <int K, int PPL, bool NARROW, bool STATS>
+template <int K, int PPL, bool NARROW, bool STATS, bool CHECK>
 __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl, const uint2* rinfo, uint32_t* rcnt,
                                             uint32_t* ecnt, const uint8_t* rep_of, int l, int p0, int nrep,
                                             bool counter, uint32_t t_begin, uint32_t t_end, uint32_t off_f,
-                                            uint32_t hs, uint32_t hz, int f, uint32_t& err,
+                                            uint32_t hs, uint32_t hz, int f,
                                             uint32_t (&acc_span)[PPL], uint32_t (&acc_home)[PPL],
                                             uint32_t (&acc_cross)[PPL], uint32_t& n_scored) {
   using S = Scorer<K, PPL, NARROW, STATS>;
@@ -422,7 +470,6 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
   const int E = a.E, G = a.G, L = a.L;
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  uint32_t n_bad = 0;  // invalid token-layers met by this wave (wave-uniform)
   const int nwaves = blockDim.x >> 6;
   const int16_t* trace_l = a.trace + static_cast<int64_t>(l) * a.N * K;
   S sc;
@@ -445,6 +492,14 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
       uint32_t pk[KB];
 #pragma unroll
       for (int w = 0; w < KB; ++w) pk[w] = 0;
+      // does the tile meet a group of 64 flattened token-layers that ev_valid marked? (wave-uniform;
+      // only the variant for traces with an invalid token-layer reads the marks)
+      bool marked = false;
+      if constexpr (CHECK) {
+        const int64_t x0 = static_cast<int64_t>(l) * a.N + tile;
+        const int64_t g0 = x0 >> 6, g1 = min(x0 + 63, static_cast<int64_t>(L) * a.N - 1) >> 6;
+        marked = (((a.ws.bad_tiles[g0 >> 5] >> (g0 & 31)) | (a.ws.bad_tiles[g1 >> 5] >> (g1 & 31))) & 1u) != 0u;
+      }
       uint32_t info = 0;
       bool bad = false;
       if (t < r_end) {
@@ -452,12 +507,10 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
         uint32_t raw[K];
 #pragma unroll
         for (int s = 0; s < K; ++s) raw[s] = static_cast<uint16_t>(idp[s]);
-        bool ok = true;
         int nth = 0;
 #pragma unroll
         for (int s = 0; s < K; ++s) {
           const uint32_t id = min(raw[s], static_cast<uint32_t>(E - 1));
-          ok &= raw[s] < static_cast<uint32_t>(E);
           const uint32_t r = rep_of[id];
           if (r != kNone) {
             info |= 1u << s;
@@ -467,28 +520,28 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
           pk[s >> 2] |= id << (8 * (s & 3));
         }
         info |= ((t - off_f) % hz) << IL::kHomeShift;
-        bool dup = false;
+        if (marked) {
+          // an invalid token-layer (flagged by ev_valid) is not scored; its ids stay clamped in
+          // range, unused
+          bool ok = true, dup = false;
 #pragma unroll
-        for (int s = 1; s < K; ++s)
+          for (int s = 0; s < K; ++s) {
+            ok &= raw[s] < static_cast<uint32_t>(E);
 #pragma unroll
-          for (int q = 0; q < s; ++q) dup |= raw[s] == raw[q];
-        // an invalid token-layer is flagged and not scored (its ids stay clamped in range, unused)
-        bad = !ok || dup;
-        if (bad) info = IL::kBad;
-        if (counter) {
-          if (!ok) err |= TACG_ERR_ID_RANGE;
-          if (dup) err |= TACG_ERR_ID_DUP;
-          if (!bad) {
-#pragma unroll
-            for (int s = 0; s < K; ++s)
-              __hip_atomic_fetch_add(&ecnt[raw[s]], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            for (int q = 0; q < s; ++q) dup |= raw[s] == raw[q];
           }
+          bad = !ok || dup;
+          if (bad) info = IL::kBad;
+        }
+        if (counter && !bad) {
+#pragma unroll
+          for (int s = 0; s < K; ++s)
+            __hip_atomic_fetch_add(&ecnt[raw[s]], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
       }
       const uint32_t ntile = min(64u, r_end - tile);
       const uint32_t nbad = static_cast<uint32_t>(__builtin_popcountll(__builtin_amdgcn_ballot_w64(bad)));
       n_scored += ntile - nbad;
-      n_bad += nbad;
       uint32_t j = 0;
       if (nbad == 0u) {  // wave-uniform: a tile with invalid token-layers takes the loop below
         for (; j + U <= ntile; j += U) {
@@ -537,8 +590,6 @@ __device__ __forceinline__ void score_piece(const EvArgs& a, const uint32_t* tbl
       __syncthreads();
     }
   }
-  // the workgroups of placement block 0 see every token-layer once: they count the invalid ones
-  if (counter && n_bad != 0u && lane == 0) atomicAdd(a.ws.n_bad, static_cast<unsigned long long>(n_bad));
   if (nrep > 0) {  // one global add per counter and workgroup
 #pragma unroll
     for (int c = 0; c < kRcntPerThread; ++c) {
@@ -644,16 +695,25 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
   __syncthreads();
 
   const int lane = threadIdx.x & 63;
-  uint32_t err = 0;
+  // ev_valid counted the invalid token-layers: almost always none, and then no tile checks its ids
+  const bool any_bad = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(*a.ws.n_bad != 0u)) != 0u;
 
   uint32_t acc_span[PPL], acc_home[PPL], acc_cross[PPL];
   uint32_t n_scored = 0;  // token-layers scored by this wave
-  if (hz <= 4) {
-    score_piece<K, PPL, true, STATS>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end, off_f,
-                                     hs, hz, f, err, acc_span, acc_home, acc_cross, n_scored);
+  if (any_bad) {  // a trace with invalid token-layers: the variant that checks the marked tiles
+    if (hz <= 4) {
+      score_piece<K, PPL, true, STATS, true>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end,
+                                             off_f, hs, hz, f, acc_span, acc_home, acc_cross, n_scored);
+    } else {
+      score_piece<K, PPL, false, STATS, true>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end,
+                                              off_f, hs, hz, f, acc_span, acc_home, acc_cross, n_scored);
+    }
+  } else if (hz <= 4) {
+    score_piece<K, PPL, true, STATS, false>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end,
+                                            off_f, hs, hz, f, acc_span, acc_home, acc_cross, n_scored);
   } else {
-    score_piece<K, PPL, false, STATS>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end, off_f,
-                                      hs, hz, f, err, acc_span, acc_home, acc_cross, n_scored);
+    score_piece<K, PPL, false, STATS, false>(a, tbl, rinfo, rcnt, ecnt, rep_of, l, p0, nrep, counter, t_begin, t_end,
+                                             off_f, hs, hz, f, acc_span, acc_home, acc_cross, n_scored);
   }
 
   // ---- flush: each wave adds its per-placement costs into the workgroup's LDS sums as it finishes;
@@ -688,7 +748,6 @@ __global__ __launch_bounds__(kMainThreads) void ev_main(EvArgs a) {
       }
     }
   }
-  if (err) atomicOr(a.d_err, err);
   if (counter) {
     barrier_after_lds_atomics();
     for (int i = threadIdx.x; i < E; i += blockDim.x) {
@@ -784,6 +843,11 @@ int launch_main(const EvArgs& a, int n_pblocks, hipStream_t stream) {
 
 template <int K>
 int launch_main_k(const EvArgs& a, hipStream_t stream) {
+  {
+    const int64_t groups = (a.N * a.L + 63) / 64;  // one wave per 64 token-layers, four waves per block
+    const int blocks = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(8192, (groups + 3) / 4)));
+    hipLaunchKernelGGL(ev_valid<K>, dim3(blocks), dim3(256), 0, stream, a);
+  }
   // the statistics variant exists for two placements per lane only (it is not on the timed path)
   if (a.stats) return launch_main<K, 2, true>(a, (a.P + 127) / 128, stream);
   if (a.E > 64) return launch_main<K, 2, false>(a, (a.P + 127) / 128, stream);
@@ -853,9 +917,8 @@ __global__ __launch_bounds__(64) void jain_kernel(const uint32_t* __restrict__ l
 }  // namespace
 
 size_t eval_workspace(int64_t n_tokens, int32_t L, int32_t E, int32_t G, int32_t P, int32_t F) {
-  (void)n_tokens;
   size_t used = 0;
-  carve_ev(nullptr, L, E, G, P, F, &used);
+  carve_ev(nullptr, n_tokens, L, E, G, P, F, &used);
   return used;
 }
 
@@ -871,7 +934,7 @@ int launch_eval(const int16_t* trace, int64_t N, int32_t L, int32_t K, int32_t E
   a.secondary = R > 0 ? secondary : nullptr;
   a.load_ref = load_ref;
   a.d_err = d_err;
-  a.ws = carve_ev(workspace, L, E, G, P, F);
+  a.ws = carve_ev(workspace, N, L, E, G, P, F);
   a.N = N;
   a.L = L;
   a.K = K;
