@@ -18,10 +18,11 @@
  *   oracle_score_online   -- the same with the guard and the least-loaded choice reading decayed
  *                            per-GPU loads updated after every token (Sec. 3.4 eq. load-update).
  *
- * Parity unpinned: the order of preference among several feasible candidates (below) is a reading
- * of Sec. 3.4, which names the ingredients (reached GPUs, the anchor, the loads) but not a rule; the
- * tests pin this implementation of the reading with hand-built cases and independent brute force,
- * not with values printed in the paper.
+ * The order of preference among several feasible candidates (below) is a reading of Sec. 3.4, which
+ * names the ingredients (reached GPUs, the anchor, the loads) but prints no rule or worked value for
+ * it.  The tests pin this implementation of the reading with hand-built cases, invariants (GPU
+ * relabelling, a single GPU, no replicas, every expert at home) and a separate brute force in exact
+ * rational arithmetic; no printed value of the paper bears on it.
  *
  * Readings taken where the paper is silent (each also used by the HIP path, written separately):
  *   - a token whose ids repeat or fall outside [0, E) is an input error: it is flagged and skipped;
