@@ -317,6 +317,44 @@ def test_eval_invalid_ids_not_scored(name, setidx, n_place):
     _score_both(w, w.placement_sets[setidx], cfg.E, tr=tr, expect_err=tacg.ERR_ID_RANGE | tacg.ERR_ID_DUP)
 
 
+def _plant_dense_invalid(tr, E, fam_off):
+    """A copy of trace tr where invalid token-layers are the rule in places: every token-layer of
+    layer 1 out of range, every token-layer of the second family repeats an id, and a run of 200
+    token-layers of layer 0 across several groups of 64 with a negative id."""
+    tr = tr.clone()
+    L, N, k = tr.shape
+    tr[1 % L, :, 0] = E
+    f0, f1 = int(fam_off[1]), int(fam_off[2])
+    tr[:, f0:f1, k - 1] = tr[:, f0:f1, 0]
+    tr[0, 200:400, k // 2] = -5
+    return tr
+
+
+@pytest.mark.parametrize("name,n_place", [("tiny", 16), ("deepseek16b", 130), ("deepseek_v3", 65)])
+def test_eval_dense_invalid_ids_not_scored(name, n_place):
+    """Whole layers, whole families and long runs of invalid token-layers: every tile of some layers
+    is skipped, and costs, loads and per-family costs still equal the oracle's."""
+    cfg = synth.CONFIGS[name]
+    n = cfg.tokens_group if name == "tiny" else cfg.F * 700 + 37
+    w = synth.make_workload(name, device="cuda", n_tokens=n, layers=min(cfg.L, 3), n_place=n_place)
+    _say(f"eval dense invalid ids {name} P={n_place}")
+    tr = _plant_dense_invalid(w.trace_serve, cfg.E, w.fam_off_serve)
+    _score_both(w, w.placement_sets[0], cfg.E, tr=tr, expect_err=tacg.ERR_ID_RANGE | tacg.ERR_ID_DUP)
+
+
+def test_eval_every_id_invalid():
+    """A trace with no valid token-layer: nothing is scored (zero costs and loads), and both error
+    bits are raised."""
+    cfg = synth.CONFIGS["deepseek_v3"]
+    w = synth.make_workload("deepseek_v3", device="cuda", n_tokens=16 * 300 + 5, layers=2, n_place=65)
+    tr = w.trace_serve.clone()
+    tr[0, :, 0] = cfg.E
+    tr[1, :, 1] = tr[1, :, 0]
+    _say("eval every id invalid")
+    out, _ = _score_both(w, w.placement_sets[0], cfg.E, tr=tr, expect_err=tacg.ERR_ID_RANGE | tacg.ERR_ID_DUP)
+    assert int(out["cost_span"].abs().sum()) == 0 and int(out["load"].abs().sum()) == 0
+
+
 @pytest.mark.parametrize("band", [1, 2, 4, 8])
 def test_eval_band_widths(band):
     """Anchor bands of 1, 2, 4 (fallbacks packed per band position) and 8 GPUs (tested per token),

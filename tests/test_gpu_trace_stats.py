@@ -94,10 +94,12 @@ def test_trace_stats_presets(name, setidx, n_place):
           ps["secondary"])
 
 
-@pytest.mark.parametrize("name,n_place", [("deepseek16b", 130), ("deepseek_v3", 65)])
-def test_trace_stats_invalid_ids_not_counted(name, n_place):
+@pytest.mark.parametrize("name,n_place,dense", [("deepseek16b", 130, False), ("deepseek_v3", 65, False),
+                                                ("deepseek_v3", 65, True)])
+def test_trace_stats_invalid_ids_not_counted(name, n_place, dense):
     """Token-layers with an id out of range or a repeated id are flagged and left out of every
-    statistic, cost and load, as in the oracle."""
+    statistic, cost and load, as in the oracle: scattered ones, and (dense) a whole layer, a whole
+    family and a run of 200 token-layers."""
     cfg = synth.CONFIGS[name]
     w = synth.make_workload(name, n_tokens=cfg.F * 900 + 37, layers=2, n_place=n_place)
     ps = w.placement_sets[0]
@@ -108,7 +110,12 @@ def test_trace_stats_invalid_ids_not_counted(name, n_place):
         l, t, s = int(rng.integers(L)), int(rng.integers(N)), int(rng.integers(k))
         tr[l, t, s] = [cfg.E, -7, int(tr[l, t, (s + 1) % k])][i % 3]
     tr[:, 64:68, 0] = cfg.E   # a whole group of four
-    _say(f"trace stats invalid ids {name}")
+    if dense:
+        tr[1, :, 0] = cfg.E
+        f0, f1 = int(w.fam_off_serve[1]), int(w.fam_off_serve[2])
+        tr[:, f0:f1, k - 1] = tr[:, f0:f1, 0]
+        tr[0, 200:400, k // 2] = -5
+    _say(f"trace stats invalid ids {name} dense={dense}")
     _both(tr, w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], ps["n_gpus"], ps["primary"],
           ps["secondary"], expect_err=tacg.ERR_ID_RANGE | tacg.ERR_ID_DUP)
 
