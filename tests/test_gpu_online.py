@@ -124,9 +124,11 @@ def test_online_state_carry_and_initial_state():
     np.testing.assert_array_equal(st.cpu().numpy(), whole["state"].cpu().numpy())
 
 
-def test_online_invalid_ids_not_served():
+@pytest.mark.parametrize("dense", [False, True])
+def test_online_invalid_ids_not_served(dense):
     """Token-layers with an id out of range or a repeated id are flagged, not served and leave the
-    decayed loads untouched, as in the oracle: every output, the final loads included, is equal."""
+    decayed loads untouched, as in the oracle: every output, the final loads included, is equal.
+    Dense: also a whole layer, a whole family and a run of 200 token-layers."""
     cfg = synth.CONFIGS["deepseek_v3"]
     w = synth.make_workload("deepseek_v3", n_tokens=16 * 300 + 11, layers=2, n_place=70)
     ps = w.placement_sets[0]
@@ -136,7 +138,12 @@ def test_online_invalid_ids_not_served():
     for i in range(24):
         l, t, s = int(rng.integers(L)), int(rng.integers(N)), int(rng.integers(k))
         tr[l, t, s] = [cfg.E, -2, int(tr[l, t, (s + 1) % k])][i % 3]
-    _say("online invalid ids")
+    if dense:
+        tr[1, :, 0] = cfg.E
+        f0, f1 = int(w.fam_off_serve[1]), int(w.fam_off_serve[2])
+        tr[:, f0:f1, k - 1] = tr[:, f0:f1, 0]
+        tr[0, 200:400, k // 2] = -5
+    _say(f"online invalid ids dense={dense}")
     _both(tr, w.fam_off_serve, cfg.E, ps["home_start"], ps["home_size"], ps["n_gpus"], ps["primary"],
           ps["secondary"], 0.995, (3, 20), expect_err=tacg.ERR_ID_RANGE | tacg.ERR_ID_DUP)
 

@@ -181,6 +181,26 @@ def test_coact_data_errors_flagged(E, k):
         np.testing.assert_array_equal(_u32(D), Do)
 
 
+@pytest.mark.parametrize("E,k", [(16, 3), (64, 6), (60, 4), (128, 8), (100, 10), (96, 6), (256, 8), (200, 6)])
+def test_coact_dense_invalid(E, k):
+    """Invalid token-layers as the rule in places (histogram and matrix-core paths): a whole segment
+    out of range, a whole segment with repeated ids, and a run of 300 token-layers across several
+    batches of 64; the valid rest is counted exactly as the oracle counts it."""
+    off = [0, 1500, 2900, 4100]
+    tr = _rand_trace(2, off[-1], k, E, 29)
+    tr[1, off[0]:off[1], 0] = E
+    tr[0, off[1]:off[2], k - 1] = tr[0, off[1]:off[2], 0]
+    tr[1, 2950:3250, k // 2] = -1
+    _say(f"coact dense invalid E={E} k={k} matrix={tacg.coact_uses_matrix_cores(E, k)}")
+    D, C, err = tacg.coact_build(tr, off, E)
+    assert _err(err) == tacg.ERR_ID_RANGE | tacg.ERR_ID_DUP
+    Do, Co, eo = oracle.coact(tr.cpu(), off, E)
+    assert eo == tacg.ERR_ID_RANGE | tacg.ERR_ID_DUP
+    np.testing.assert_array_equal(_u32(D), Do)
+    np.testing.assert_array_equal(_u32(C), Co)
+    assert int(Do[0, 1].sum()) == 0 and int(Do[1, 0].sum()) == 0
+
+
 @pytest.mark.parametrize("E,k", [(16, 4), (16, 6), (64, 8), (100, 8), (256, 8)])
 def test_coact_empty_trace(E, k):
     tr = torch.zeros((2, 0, k), dtype=torch.int16, device="cuda")
