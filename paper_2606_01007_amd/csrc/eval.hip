@@ -311,7 +311,8 @@ __global__ __launch_bounds__(256) void ev_repinfo(EvArgs a) {
 // The trace pass.  PPL placements per lane (one 8- or 16-byte LDS read per slot serves all of them);
 // a workgroup scores 64 * PPL placements of one layer on one piece of one family's tokens.
 // grid (placement blocks, pieces, L).  The workgroups of placement block 0 also count the
-// dispatches of every expert and validate the ids (each token-layer is seen by exactly one of them).
+// dispatches of every expert (each token-layer is seen by exactly one of them); ev_valid has already
+// checked the ids, and only tiles it marked check them again, to leave their invalid token-layers out.
 // Choices for replicated experts are counted in 16-bit LDS counters (two per dword).  After every
 // round of at most 65535 / K tokens (so that they cannot overflow) each thread adds a fixed set of
 // them into 32-bit registers and clears them; the registers go to the workspace once per workgroup.
