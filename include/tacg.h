@@ -204,7 +204,8 @@ size_t tacg_eval_workspace_bytes(int64_t n_tokens, int32_t n_layers, int32_t n_e
  * or threads enqueueing at once) race on it and give unspecified results; serialise them.
  * Returns TACG_E_SCRATCH, before anything is enqueued, when tacg_eval_workspace_bytes(...) of the
  * arguments exceeds TACG_NOALLOC_SCRATCH_BYTES (at E = 256, L = 58, G = 32 and F = 16 it holds about
- * 2100 placements); TACG_E_DEVICE if the scratch address cannot be obtained.
+ * 2100 placements on short traces and 2050 on a trace of 2^23 tokens, whose validation marks take
+ * one bit per token-layer); TACG_E_DEVICE if the scratch address cannot be obtained.
  */
 int tacg_eval_placements_noalloc(const int16_t* trace, int64_t n_tokens, int32_t n_layers, int32_t top_k,
                                  int32_t n_experts, const int64_t* fam_off_host, int32_t n_fam,
