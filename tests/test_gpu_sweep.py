@@ -11,6 +11,7 @@ to 60,000 tokens (some nearly empty), so that several co-activation workgroups m
 boundaries and the scoring kernel runs many pieces.  Counts, costs, loads and the final float64
 loads are compared exactly; float outputs within the tolerances of the other parity tests.
 """
+import os
 import sys
 
 import numpy as np
@@ -83,12 +84,17 @@ def _draw_large(seed):
     return dict(E=E, k=k, L=L, counts=counts, G=G, cap=cap, P=P, R=R, n_rep=n_rep, theta=theta, rho=rho)
 
 
-@pytest.mark.parametrize("seed", range(256))
+# seeds drawn: 256 and 16 by default; TACG_SWEEP_SMALL / TACG_SWEEP_LARGE widen the sweep
+N_SMALL = int(os.environ.get("TACG_SWEEP_SMALL", "256"))
+N_LARGE = int(os.environ.get("TACG_SWEEP_LARGE", "16"))
+
+
+@pytest.mark.parametrize("seed", range(N_SMALL))
 def test_random_shape_sweep(seed):
     _check(_draw(seed), seed)
 
 
-@pytest.mark.parametrize("seed", range(16))
+@pytest.mark.parametrize("seed", range(N_LARGE))
 def test_random_large_shape_sweep(seed):
     _check(_draw_large(seed), seed)
 
