@@ -11,6 +11,7 @@ scoring.  Every other output is checked through
 properties that hold at any size (symmetry, diagonal, row sums and totals of the counts; per-layer
 load totals and cost bounds of the scores).
 """
+import os
 import sys
 import time
 
@@ -62,6 +63,10 @@ def sampled_placements(P: int, n_experts: int):
     pb = 64 * ppl
     want = {0, 1, 2, 3, 37, 2 * 37 + 1, pb - 2, pb - 1, pb, pb + 1, P // 2 + 5, P // 2 + 70, (3 * P) // 4 + 43,
             P - 2, P - 1}
+    if os.environ.get("TACG_FULLSIZE_BLOCKS"):
+        # opt-in (minutes of oracle time per preset): the whole first placement block, every lane and
+        # every position within a lane, and the last 64 placements
+        want |= set(range(pb)) | set(range(P - 64, P))
     return sorted(p for p in want if 0 <= p < P)
 
 
