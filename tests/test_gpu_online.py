@@ -64,6 +64,17 @@ def test_hand_worked_alternation():
     np.testing.assert_array_equal(out["state"].cpu().numpy()[0, 0], [21 / 16, 5 / 8, 0.0])
 
 
+def test_guard_boundary_is_inclusive():
+    """A GPU whose decayed load equals (1 + theta) times the mean stays feasible (loads (2, 1, 0),
+    theta = 0): the token's replicated expert joins the GPU it already reaches."""
+    tr = np.array([[[0, 1]]], dtype=np.int16)
+    prim = np.array([[[1, 2, 0, 0]]], dtype=np.uint8)
+    sec = np.array([[[[0xFF], [1], [0xFF], [0xFF]]]], dtype=np.uint8)
+    st = np.array([[[2.0, 1.0, 0.0]]])
+    out, _ = _both(tr, [0, 1], 4, [0], [1], 3, prim, sec, 0.5, (0, 1), state=st)
+    np.testing.assert_array_equal(tacg.as_u32(out["load"]).cpu().numpy()[0, 0], [0, 2, 0])
+
+
 @pytest.mark.parametrize("E,k,L,counts,G,cap,n_rep,R,P,rho,theta,seed", [
     (16, 8, 2, [700, 0, 513], 4, 4, 16, 2, 20, 0.995, (3, 20), 1),     # every expert replicated
     (16, 16, 1, [300, 301], 8, 2, 16, 3, 9, 0.9, (3, 20), 2),          # k = 16 (8-bit dispatch counts)

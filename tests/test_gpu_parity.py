@@ -375,6 +375,24 @@ def test_eval_every_id_invalid():
     assert int(out["cost_span"].abs().sum()) == 0 and int(out["load"].abs().sum()) == 0
 
 
+def test_eval_guard_boundary_is_inclusive():
+    """Snapshot guard: a GPU whose load equals (1 + theta) times the mean stays feasible (loads
+    (2, 1, 0), theta = 0), so the replicated expert joins the GPU the token already reaches."""
+    tr = torch.tensor([[[0, 1]]], dtype=torch.int16, device="cuda")
+    prim = np.array([[[1, 2, 0, 0]]], dtype=np.uint8)
+    sec = np.array([[[[0xFF], [1], [0xFF], [0xFF]]]], dtype=np.uint8)
+    ref = np.array([[[2, 1, 0]]], dtype=np.int64)
+    out = tacg.eval_placements(tr, [0, 1], 4, [0], [1], 3, torch.as_tensor(prim).cuda(), torch.as_tensor(sec).cuda(),
+                               torch.as_tensor(ref).cuda(), theta=(0, 1))
+    assert _err(out["err"]) == 0
+    ro = oracle.score(tr.cpu(), [0, 1], 4, [0], [1], 3, prim, sec, ref, (0, 1))
+    assert ro["err"] == 0
+    np.testing.assert_array_equal(_u32(out["load"]), ro["load"])
+    np.testing.assert_array_equal(ro["load"][0, 0], [0, 2, 0])
+    assert int(out["cost_span"][0]) == int(ro["cost_span"][0]) == 0
+    assert int(out["cost_home"][0]) == int(ro["cost_home"][0]) == 1
+
+
 @pytest.mark.parametrize("band", [1, 2, 4, 8])
 def test_eval_band_widths(band):
     """Anchor bands of 1, 2, 4 (fallbacks packed per band position) and 8 GPUs (tested per token),

@@ -57,6 +57,23 @@ def test_initial_state_steers_first_choice(oracle_mod):
     np.testing.assert_array_equal(r["state"][0, 0], [2.5, 1.5, 0.0])
 
 
+def test_guard_boundary_is_inclusive(oracle_mod):
+    # eq. feasible-set keeps a GPU whose load equals (1 + theta) times the mean.  G = 3, theta = 0,
+    # loads (2, 1, 0): mean 1, so GPU 1 sits on the boundary (feasible), GPU 2 below it, GPU 0 above.
+    # One token picks expert 0 (only on GPU 1, so GPU 1 is reached) and expert 1 (candidates GPU 2 and
+    # GPU 1): the lowest reached feasible candidate is GPU 1, and the token stays on one GPU.  Were
+    # the boundary excluded, expert 1 would go to GPU 2 and the token would span two GPUs.
+    tr = np.array([[[0, 1]]], dtype=np.int16)
+    prim = np.array([[[1, 2, 0, 0]]], dtype=np.uint8)
+    sec = np.array([[[[0xFF], [1], [0xFF], [0xFF]]]], dtype=np.uint8)
+    st = np.array([[[2.0, 1.0, 0.0]]])
+    r = oracle_mod.score_online(tr, [0, 1], 4, [0], [1], 3, prim, sec, rho=0.5, theta=(0, 1), state=st)
+    assert r["err"] == 0
+    np.testing.assert_array_equal(r["load"][0, 0], [0, 2, 0])
+    assert r["cost_span"][0] == 0 and r["cost_home"][0] == 1
+    np.testing.assert_array_equal(r["state"][0, 0], [1.0, 2.5, 0.0])
+
+
 def test_without_replicas_equals_snapshot_rule(oracle_mod):
     w = synth.make_workload("qwen15", n_tokens=3000, n_place=5, layers=2)
     ps = w.placement_sets[0]
