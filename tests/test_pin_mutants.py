@@ -29,7 +29,16 @@ MUTANTS = [
     ("diagonal left at zero", C, "C[(int64_t)i * E + i] = D[i];", "C[(int64_t)i * E + i] = 0;", 0, ["counts"]),
     ("repeated ids accepted", C, "if (ids[s] == ids[s2]) err |= ORC_ERR_ID_DUP;", "if (0) err |= ORC_ERR_ID_DUP;", 0,
      ["counts"]),
+    ("last token of every family dropped", C, "l, fam_off[f], fam_off[f + 1],",
+     "l, fam_off[f], fam_off[f + 1] - (fam_off[f + 1] > fam_off[f]),", 0, ["counts"]),
     # ---- snapshot scoring (Sec. 3.4, App. C, App. H) ----
+    ("loads of the first slot only", C, "for (int32_t s = 0; s < k; ++s) ld[slot_gpu[s]] += 1;",
+     "for (int32_t s = 0; s < k; ++s) ld[slot_gpu[0]] += 1;", 0, ["score"]),
+    ("single-candidate GPUs not reached first", C,
+     "if (n_cand[e] == 1) { slot_gpu[s] = cand[e][0]; in_r[cand[e][0]] = 1; }",
+     "if (n_cand[e] == 1) { slot_gpu[s] = cand[e][0]; }", 0, ["score"]),
+    ("band test off by one", C, "if (in_r[m] && (m < home_start[f2] || m >= home_start[f2] + home_size[f2]))",
+     "if (in_r[m] && (m < home_start[f2] || m > home_start[f2] + home_size[f2]))", 0, ["score"]),
     ("guard strict", C, "feas[m] = lhs <= rhs;", "feas[m] = lhs < rhs;", 0, ["score"]),
     ("guard without theta", C, "__int128 rhs = (__int128)(theta_den + theta_num) * total;",
      "__int128 rhs = (__int128)theta_den * total;", 0, ["score"]),
@@ -69,7 +78,14 @@ MUTANTS = [
     ("decayed: span counts every card", C, "span_acc += n_cards - 1;", "span_acc += n_cards;", 1, ["online"]),
     ("decayed: home cost counts the anchor", C, "int64_t home_cost = n_cards - in_r[h];",
      "int64_t home_cost = n_cards;", 1, ["online"]),
+    ("guard sum misses the last GPU", C, "for (int32_t m = 0; m < G; ++m) S += Lm[m];",
+     "for (int32_t m = 0; m < G - 1; ++m) S += Lm[m];", 0, ["online"]),
     # ---- preferences and graph (Sec. 3.3) ----
+    ("self pairs kept in A", PY, "np.fill_diagonal(A[f], 0.0)", "pass", 0, ["reweight"]),
+    ("softmax over experts", PY, "w = np.exp(z - z.max(axis=0, keepdims=True))\n    p = w / w.sum(axis=0, keepdims=True)",
+     "w = np.exp(z - z.max(axis=1, keepdims=True))\n    p = w / w.sum(axis=1, keepdims=True)", 0, ["reweight"]),
+    ("graph normalised by its sum", PY, "ah = a_bar / mx if mx > 0 else np.zeros((E, E))",
+     "ah = a_bar / a_bar.sum() if mx > 0 else np.zeros((E, E))", 0, ["reweight"]),
     ("sample standard deviation", PY, "sigma = np.sqrt(((x - mu) ** 2).mean())",
      "sigma = np.sqrt(((x - mu) ** 2).sum() / max(x.size - 1, 1))", 0, ["reweight"]),
     ("usage without the factor k", PY, "u[f] = D_l[f] / (n_f * top_k)", "u[f] = D_l[f] / n_f", 0,
@@ -81,6 +97,8 @@ MUTANTS = [
     # ---- snapshot loads, Jain and MaxVio (App. H) ----
     ("snapshot loads of one family", PY, "out[p, l, prim[p, l, e]] += dsum[l, e]",
      "out[p, l, prim[p, l, e]] += D[0, l, e]", 0, ["score"]),
+    ("Jain of the first layer only", PY, "return jain_maxvio(ld.sum(axis=1))", "return jain_maxvio(ld[:, 0])", 0,
+     ["jain"]),
     ("Jain without G", PY, "tot ** 2 / (G * sq)", "tot ** 2 / sq", 0, ["jain"]),
     ("MaxVio over the total", PY, "(Lm.max(axis=-1) - mean) / mean", "(Lm.max(axis=-1) - mean) / tot", 0,
      ["jain"]),
@@ -89,12 +107,17 @@ MUTANTS = [
      "cs += float(A[f, e] @ a_bar[e])", 0, ["gesr_scores"]),
     ("specificity summed", PY, "worst = max(worst, float(np.sqrt(((A[f, e] - a_bar[e]) ** 2).sum())))",
      "worst = worst + float(np.sqrt(((A[f, e] - a_bar[e]) ** 2).sum()))", 0, ["gesr_scores"]),
+    ("centrality of one family", PY, "cent[l, e] = a_bar[e].sum()", "cent[l, e] = A[0, e].sum()", 0,
+     ["gesr_scores"]),
     ("objective over unordered pairs", PY, "if e2 != e:", "if e2 > e:", 0, ["objective"]),
     # ---- motivation diagnostics (App. H) ----
     ("activation probability without k", PY, "n = D[f, l].sum() / top_k", "n = D[f, l].sum()", 0,
      ["diagnostics"]),
     ("Jaccard over the larger set", PY, "out[l, i, j] = len(a & b) / u if u else 1.0",
      "out[l, i, j] = len(a & b) / max(len(a), len(b)) if u else 1.0", 0, ["diagnostics"]),
+    ("activation distance in L1", PY, "dist[i, j] = np.sqrt(((Pm[i] - Pm[j]) ** 2).sum())",
+     "dist[i, j] = np.abs(Pm[i] - Pm[j]).sum()", 0, ["diagnostics"]),
+    ("zero-count pairs ranked", PY, "keep = cnt > 0", "keep = cnt >= 0", 0, ["diagnostics"]),
     ("top pairs ties to the higher index", PY, "np.lexsort((idx[keep], -cnt[keep]))",
      "np.lexsort((-idx[keep], -cnt[keep]))", 0, ["diagnostics"]),
 ]
